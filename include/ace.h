@@ -1,0 +1,135 @@
+/*
+ * ace.h — C ABI of the ACE token-adaptive MoE layer for AMD Instinct MI355X (gfx950).
+ *
+ * The library computes one MoE layer forward with ACE's calibration-free expert
+ * skipping (arxiv 2609.05228): RMSNorm, router logits, softmax/top-k with gate
+ * renormalisation, the ACE skip mask (Alg. 4, "ACE: Online Conservative Expert
+ * Skipping"), and the sparsified output y_t = sum_{i in I_t} ghat_i f_{e_i}(x_t)
+ * (Eq. ace_sparse_output), where f_e is the SwiGLU expert of Eq. swiglu_expert.
+ * The per-expert GSP and RCR amplification tables (Alg. 2, Alg. 3) and the
+ * threshold tau (App. C.1) are inputs: "per-expert statistics in, layer input and
+ * weights in, output plus skip mask out".
+ *
+ * Conventions for every entry point
+ *   - Pointers marked DEVICE are device (HBM) pointers; the caller owns every
+ *     buffer.  The library allocates nothing and keeps no per-call state.
+ *   - Descriptor, weight and output structs are HOST structs passed by pointer;
+ *     they are read during the call only.
+ *   - ace_moe_forward validates everything on the host before any launch; on an
+ *     error nothing is enqueued and the returned status says why.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and the
+ *     call returns without synchronising the host.
+ *   - All arrays are dense row-major with the layouts stated below; every device
+ *     pointer must be 16-byte aligned.
+ */
+#ifndef ACE_H
+#define ACE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ACE_ABI_VERSION 1
+
+typedef enum {
+  ACE_OK = 0,
+  ACE_ERR_INVALID_ARG = -1, /* NULL required pointer, bad shape, misaligned pointer, bad scalar */
+  ACE_ERR_UNSUPPORTED = -2, /* valid but outside the compiled shape/dtype set (see ace_moe_forward) */
+  ACE_ERR_WORKSPACE = -3,   /* workspace NULL or smaller than ace_moe_workspace_size() */
+  ACE_ERR_HIP = -4          /* a HIP launch reported an error */
+} ace_status;
+
+typedef enum { ACE_F32 = 0, ACE_BF16 = 1 } ace_dtype;
+
+enum {
+  /* Plain top-k layer through the same kernels: every routed slot is kept and
+     ghat = g exactly (no epsilon).  This is the unskipped baseline. */
+  ACE_SKIP_DISABLE = 1u << 0,
+  /* Fill outputs.scores with the ACE contribution c = max(p_GSP, p_RCR)
+     (Eq. ace_contribution) of every routed slot, as the App. C.1 score pass needs. */
+  ACE_WRITE_SCORES = 1u << 1
+};
+
+/* Layer shape and the scalars of Alg. 4. */
+typedef struct {
+  int32_t T;        /* tokens (0 = nothing to do) */
+  int32_t d;        /* hidden size */
+  int32_t N;        /* routed experts */
+  int32_t k;        /* top-k */
+  int32_t m;        /* expert intermediate size */
+  int32_t n_shared; /* 0 or 1 ungated, always-active shared expert (not a routed slot) */
+  int32_t m_shared; /* its intermediate size (ignored when n_shared = 0) */
+  int32_t dtype;    /* ace_dtype of x, gamma, every weight matrix and y */
+  int32_t m_min;    /* minimum active experts per token, 1..k (1 = top-1 safeguard only) */
+  float tau;        /* threshold tau_q; a slot is skippable iff c < tau (strict) */
+  float eps;        /* epsilon of Alg. 4 (both score normalisations and the gate renormalisation) */
+  float rms_eps;    /* RMSNorm epsilon: x_in = x / sqrt(mean(x^2) + rms_eps) * gamma */
+  uint32_t flags;   /* ACE_SKIP_DISABLE | ACE_WRITE_SCORES */
+} ace_moe_desc;
+
+/* Frozen layer parameters (DEVICE pointers, dtype = desc.dtype unless stated). */
+typedef struct {
+  const void *gamma;     /* [d]      RMSNorm scale (the diagonal of Gamma_l, Sec. 3.1)        */
+  const void *w_router;  /* [N, d]   row e is the router vector w_e (Eq. app_router_logit)     */
+  const float *b_router; /* [N] fp32 router bias b_e, or NULL for none                       */
+  const void *w_gate;    /* [N, m, d] per-expert gate projection (nn.Linear out x in layout)  */
+  const void *w_up;      /* [N, m, d] per-expert up projection                               */
+  const void *w_down;    /* [N, d, m] per-expert down projection                             */
+  const void *ws_gate;   /* [m_shared, d] shared-expert gate, or NULL when n_shared = 0       */
+  const void *ws_up;     /* [m_shared, d]                                                    */
+  const void *ws_down;   /* [d, m_shared]                                                    */
+  const float *a_gsp;    /* [N] fp32 A^GSP(e), Alg. 2 output (Eq. gsp_layer_normalization)   */
+  const float *a_rcr;    /* [N] fp32 A^RCR(e), Alg. 3 output (Eq. rcr_layer_normalization)   */
+} ace_moe_weights;
+
+/* Outputs (DEVICE pointers).  Required ones are fully overwritten; NULL optional
+   ones are skipped. */
+typedef struct {
+  void *y;                 /* [T, d] dtype, required: the layer output (Eq. ace_sparse_output) */
+  int32_t *topk_idx;       /* [T, k] required: routed experts in descending router probability;
+                              equal logits go to the lower expert id; slot 0 is the top-1 expert */
+  uint8_t *keep;           /* [T, k] required: 1 = slot in the active set I_t, 0 = skipped      */
+  float *gates;            /* [T, k] optional: ghat (renormalised gate, 0 where skipped)        */
+  float *scores;           /* [T, k] optional: c (written only with ACE_WRITE_SCORES)          */
+  int32_t *expert_counts;  /* [N]    optional: kept slots per expert                          */
+  int32_t *expert_offsets; /* [N+1]  optional: exclusive prefix sum of expert_counts          */
+  int32_t *perm;           /* [T*k]  optional: token of each kept slot in (expert, token)
+                              ascending order; entries past sum(expert_counts) are undefined */
+} ace_moe_outputs;
+
+/* Bytes of DEVICE scratch memory ace_moe_forward needs for `desc`
+   (0 if desc is NULL or T <= 0).  Depends only on the shape fields and dtype. */
+size_t ace_moe_workspace_size(const ace_moe_desc *desc);
+
+/*
+ * One ACE MoE layer forward (Alg. 1's online loop for one layer).
+ *   x          DEVICE [T, d] layer input before RMSNorm, dtype = desc->dtype.
+ *   workspace  DEVICE scratch of at least ace_moe_workspace_size(desc) bytes,
+ *              256-byte aligned; its contents on entry do not matter.  Calls that
+ *              share one workspace must be ordered on one stream.
+ *   stream     hipStream_t to enqueue on (NULL = null stream).
+ * Compiled shape set (else ACE_ERR_UNSUPPORTED): N <= 256, k <= 8, d % 128 == 0,
+ * m % 64 == 0, m_shared % 64 == 0, d <= 16384, T * k < 2^31.
+ * Semantics: tau <= 0 skips nothing (ghat = g / (1 + eps)); tau = +inf skips every
+ * slot but the top-1 (and the m_min safeguard).  Skipped slots keep their topk_idx
+ * entry and get keep = 0, ghat = 0.  Results are deterministic: two calls on the
+ * same inputs give bit-identical outputs.
+ */
+ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
+                           const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
+                           void *stream);
+
+/* Static, human-readable text of a status code (never NULL). */
+const char *ace_status_string(int status);
+
+/* ACE_ABI_VERSION of the built library. */
+int ace_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ACE_H */

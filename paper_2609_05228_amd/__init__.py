@@ -1,0 +1,14 @@
+"""ACE token-adaptive MoE layer for AMD Instinct MI355X (gfx950).
+
+The layer (RMSNorm, router, top-k, the ACE skip mask of Alg. 4, dispatch,
+grouped SwiGLU expert GEMMs and the gate-weighted combine) runs in hand-written
+HIP kernels in libace.so behind the C ABI of include/ace.h.  This package is the
+thin Python binding: `moe_forward` takes torch device tensors and enqueues the
+layer on the current HIP stream.
+"""
+from ._lib import (  # noqa: F401
+    ACE_BF16, ACE_ERR_HIP, ACE_ERR_INVALID_ARG, ACE_ERR_UNSUPPORTED, ACE_ERR_WORKSPACE, ACE_F32,
+    ACE_OK, ACE_SKIP_DISABLE, ACE_WRITE_SCORES, AceError, Desc, LIB_PATH, Outputs, Weights,
+    abi_version, forward_raw, lib, status_string, workspace_size,
+)
+from .layer import make_desc, moe_forward, workspace  # noqa: F401

@@ -1,0 +1,95 @@
+"""ctypes binding of libace.so (the C ABI declared in include/ace.h).
+
+Argument marshalling only: every step of the layer runs in the library's HIP
+kernels.  torch supplies device memory and the current HIP stream.  If the
+library is missing the import of this module still succeeds, but every call
+raises: there is no CPU or eager fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libace.so")
+
+ACE_OK = 0
+ACE_ERR_INVALID_ARG = -1
+ACE_ERR_UNSUPPORTED = -2
+ACE_ERR_WORKSPACE = -3
+ACE_ERR_HIP = -4
+ACE_F32 = 0
+ACE_BF16 = 1
+ACE_SKIP_DISABLE = 1 << 0
+ACE_WRITE_SCORES = 1 << 1
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("d", ctypes.c_int32), ("N", ctypes.c_int32),
+                ("k", ctypes.c_int32), ("m", ctypes.c_int32), ("n_shared", ctypes.c_int32),
+                ("m_shared", ctypes.c_int32), ("dtype", ctypes.c_int32), ("m_min", ctypes.c_int32),
+                ("tau", ctypes.c_float), ("eps", ctypes.c_float), ("rms_eps", ctypes.c_float),
+                ("flags", ctypes.c_uint32)]
+
+
+class Weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "gamma", "w_router", "b_router", "w_gate", "w_up", "w_down",
+        "ws_gate", "ws_up", "ws_down", "a_gsp", "a_rcr")]
+
+
+class Outputs(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "y", "topk_idx", "keep", "gates", "scores", "expert_counts", "expert_offsets", "perm")]
+
+
+class AceError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{msg} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"{LIB_PATH} is missing: build it with `python -m paper_2609_05228_amd.build` "
+                "(the ACE layer has no fallback path)")
+        L = ctypes.CDLL(LIB_PATH)
+        L.ace_moe_workspace_size.argtypes = [ctypes.POINTER(Desc)]
+        L.ace_moe_workspace_size.restype = ctypes.c_size_t
+        L.ace_moe_forward.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p, ctypes.POINTER(Weights),
+                                      ctypes.POINTER(Outputs), ctypes.c_void_p, ctypes.c_size_t,
+                                      ctypes.c_void_p]
+        L.ace_moe_forward.restype = ctypes.c_int
+        L.ace_status_string.argtypes = [ctypes.c_int]
+        L.ace_status_string.restype = ctypes.c_char_p
+        L.ace_abi_version.argtypes = []
+        L.ace_abi_version.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().ace_status_string(int(status)).decode()
+
+
+def abi_version() -> int:
+    return int(lib().ace_abi_version())
+
+
+def workspace_size(desc: Desc) -> int:
+    return int(lib().ace_moe_workspace_size(ctypes.byref(desc)))
+
+
+def forward_raw(desc: Desc, x_ptr: int, weights: Weights, outputs: Outputs, ws_ptr: int,
+                ws_bytes: int, stream: int) -> int:
+    """ace_moe_forward on plain integers/structs; returns the ace_status."""
+    return int(lib().ace_moe_forward(ctypes.byref(desc), ctypes.c_void_p(x_ptr), ctypes.byref(weights),
+                                     ctypes.byref(outputs), ctypes.c_void_p(ws_ptr),
+                                     ctypes.c_size_t(ws_bytes), ctypes.c_void_p(stream)))

@@ -1,0 +1,253 @@
+// C ABI of the ACE MoE layer: host-side validation, workspace layout and the
+// launch sequence of one layer forward (Alg. 1's online loop for one layer):
+//   zero bitmap -> route (RMSNorm, router, top-k, Alg. 4 skip mask)
+//   -> plan (histogram, prefix sum, permutation, M tiles)
+//   -> grouped gate/up + SwiGLU -> grouped down
+//   -> [shared expert: dense gate/up -> dense down] -> gate-weighted combine.
+// Everything is enqueued on the caller's stream; nothing is allocated.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/ace.h"
+#include "ace_internal.h"
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  size_t xn, bitmap, slot_row, gates, counts, offsets, perm, tile_e, tile_r0, tile_rows, n_tiles;
+  size_t H, Y, Hs, Ys, total;
+  int W, max_groups, dense_groups;
+};
+
+Layout layout_for(const ace_moe_desc &d) {
+  Layout L{};
+  const size_t T = static_cast<size_t>(d.T), dd = static_cast<size_t>(d.d);
+  const size_t N = static_cast<size_t>(d.N), k = static_cast<size_t>(d.k), m = static_cast<size_t>(d.m);
+  const size_t esz = (d.dtype == ACE_BF16) ? 2 : 4;
+  const size_t slots = T * k;
+  L.W = static_cast<int>((T + 63) / 64);
+  L.max_groups = static_cast<int>((slots + ace::kTileM - 1) / ace::kTileM + (slots < N ? slots : N));
+  L.dense_groups = static_cast<int>((T + ace::kTileM - 1) / ace::kTileM);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.xn = take(T * dd * esz);
+  L.bitmap = take(N * static_cast<size_t>(L.W) * 8);
+  L.slot_row = take(slots * 4);
+  L.gates = take(slots * 4);
+  L.counts = take(N * 4);
+  L.offsets = take((N + 1) * 4);
+  L.perm = take(slots * 4);
+  L.tile_e = take(static_cast<size_t>(L.max_groups) * 4);
+  L.tile_r0 = take(static_cast<size_t>(L.max_groups) * 4);
+  L.tile_rows = take(static_cast<size_t>(L.max_groups) * 4);
+  L.n_tiles = take(4);
+  L.H = take(slots * m * esz);
+  L.Y = take(slots * dd * esz);
+  if (d.n_shared > 0) {
+    L.Hs = take(T * static_cast<size_t>(d.m_shared) * esz);
+    L.Ys = take(T * dd * esz);
+  }
+  L.total = off;
+  return L;
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+ace_status validate(const ace_moe_desc *d, const void *x, const ace_moe_weights *w,
+                    const ace_moe_outputs *o) {
+  if (!d || !w || !o) return ACE_ERR_INVALID_ARG;
+  if (d->T < 0 || d->d <= 0 || d->N <= 0 || d->k <= 0 || d->m <= 0) return ACE_ERR_INVALID_ARG;
+  if (d->k > d->N || d->m_min < 1 || d->m_min > d->k) return ACE_ERR_INVALID_ARG;
+  if (d->dtype != ACE_F32 && d->dtype != ACE_BF16) return ACE_ERR_INVALID_ARG;
+  if (d->n_shared < 0 || d->n_shared > 1) return ACE_ERR_INVALID_ARG;
+  if (d->n_shared == 1 && d->m_shared <= 0) return ACE_ERR_INVALID_ARG;
+  if (std::isnan(d->tau) || !std::isfinite(d->eps) || d->eps < 0.f || !std::isfinite(d->rms_eps) ||
+      d->rms_eps < 0.f)
+    return ACE_ERR_INVALID_ARG;
+  if (d->flags & ~static_cast<uint32_t>(ACE_SKIP_DISABLE | ACE_WRITE_SCORES)) return ACE_ERR_INVALID_ARG;
+  if (d->N > ace::kMaxN || d->k > ace::kMaxK || d->d % 128 != 0 || d->m % 64 != 0 || d->d > 16384)
+    return ACE_ERR_UNSUPPORTED;
+  if (d->n_shared == 1 && d->m_shared % 64 != 0) return ACE_ERR_UNSUPPORTED;
+  if (static_cast<int64_t>(d->T) * d->k >= (int64_t{1} << 31)) return ACE_ERR_UNSUPPORTED;
+  if (d->T == 0) return ACE_OK;
+  const void *req[] = {x, w->gamma, w->w_router, w->w_gate, w->w_up, w->w_down, w->a_gsp, w->a_rcr,
+                       o->y, o->topk_idx, o->keep};
+  for (const void *p : req)
+    if (!p || !aligned16(p)) return ACE_ERR_INVALID_ARG;
+  if (d->n_shared == 1) {
+    const void *sreq[] = {w->ws_gate, w->ws_up, w->ws_down};
+    for (const void *p : sreq)
+      if (!p || !aligned16(p)) return ACE_ERR_INVALID_ARG;
+  }
+  const void *opt[] = {w->b_router, o->gates, o->scores, o->expert_counts, o->expert_offsets, o->perm};
+  for (const void *p : opt)
+    if (p && !aligned16(p)) return ACE_ERR_INVALID_ARG;
+  if ((d->flags & ACE_WRITE_SCORES) && !o->scores) return ACE_ERR_INVALID_ARG;
+  return ACE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t ace_moe_workspace_size(const ace_moe_desc *desc) {
+  if (!desc || desc->T <= 0 || desc->d <= 0 || desc->N <= 0 || desc->k <= 0 || desc->m <= 0) return 0;
+  return layout_for(*desc).total;
+}
+
+int ace_abi_version(void) { return ACE_ABI_VERSION; }
+
+const char *ace_status_string(int s) {
+  switch (s) {
+    case ACE_OK: return "ACE_OK: success";
+    case ACE_ERR_INVALID_ARG: return "ACE_ERR_INVALID_ARG: invalid argument (NULL, shape, alignment or scalar)";
+    case ACE_ERR_UNSUPPORTED: return "ACE_ERR_UNSUPPORTED: shape or dtype outside the compiled set";
+    case ACE_ERR_WORKSPACE: return "ACE_ERR_WORKSPACE: workspace missing or too small";
+    case ACE_ERR_HIP: return "ACE_ERR_HIP: a HIP launch failed";
+    default: return "unknown ace_status";
+  }
+}
+
+ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
+                           const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
+                           void *stream_ptr) {
+  const ace_status v = validate(desc, x, w, out);
+  if (v != ACE_OK) return v;
+  const ace_moe_desc &d = *desc;
+  if (d.T == 0) return ACE_OK;
+  const Layout L = layout_for(d);
+  if (!workspace || workspace_bytes < L.total || (reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)))
+    return ACE_ERR_WORKSPACE;
+
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  char *ws = static_cast<char *>(workspace);
+  const bool bf16 = d.dtype == ACE_BF16;
+  auto at = [&](size_t off) { return static_cast<void *>(ws + off); };
+
+  auto *bitmap = static_cast<unsigned long long *>(at(L.bitmap));
+  auto *slot_row = static_cast<int32_t *>(at(L.slot_row));
+  float *gates = out->gates ? out->gates : static_cast<float *>(at(L.gates));
+  int32_t *counts = out->expert_counts ? out->expert_counts : static_cast<int32_t *>(at(L.counts));
+  int32_t *offsets = out->expert_offsets ? out->expert_offsets : static_cast<int32_t *>(at(L.offsets));
+  int32_t *perm = out->perm ? out->perm : static_cast<int32_t *>(at(L.perm));
+  auto *tile_e = static_cast<int32_t *>(at(L.tile_e));
+  auto *tile_r0 = static_cast<int32_t *>(at(L.tile_r0));
+  auto *tile_rows = static_cast<int32_t *>(at(L.tile_rows));
+  auto *n_tiles = static_cast<int32_t *>(at(L.n_tiles));
+
+  hipError_t e = ace::launch_zero_u64(bitmap, static_cast<size_t>(d.N) * L.W, stream);
+  if (e != hipSuccess) return ACE_ERR_HIP;
+
+  ace::RouteArgs ra{};
+  ra.x = x;
+  ra.gamma = w->gamma;
+  ra.w_router = w->w_router;
+  ra.b_router = w->b_router;
+  ra.a_gsp = w->a_gsp;
+  ra.a_rcr = w->a_rcr;
+  ra.xn = at(L.xn);
+  ra.topk_idx = out->topk_idx;
+  ra.keep = out->keep;
+  ra.gates = gates;
+  ra.scores = (d.flags & ACE_WRITE_SCORES) ? out->scores : nullptr;
+  ra.slot_row = slot_row;
+  ra.bitmap = bitmap;
+  ra.T = d.T;
+  ra.d = d.d;
+  ra.N = d.N;
+  ra.k = d.k;
+  ra.m_min = d.m_min;
+  ra.W = L.W;
+  ra.tau = d.tau;
+  ra.eps = d.eps;
+  ra.rms_eps = d.rms_eps;
+  ra.skip_disable = (d.flags & ACE_SKIP_DISABLE) ? 1 : 0;
+  if (ace::launch_route(ra, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+
+  ace::PlanArgs pa{};
+  pa.bitmap = bitmap;
+  pa.topk_idx = out->topk_idx;
+  pa.counts = counts;
+  pa.offsets = offsets;
+  pa.perm = perm;
+  pa.slot_row = slot_row;
+  pa.tile_expert = tile_e;
+  pa.tile_row0 = tile_r0;
+  pa.tile_rows = tile_rows;
+  pa.n_tiles = n_tiles;
+  pa.T = d.T;
+  pa.k = d.k;
+  pa.N = d.N;
+  pa.W = L.W;
+  if (ace::launch_plan(pa, stream) != hipSuccess) return ACE_ERR_HIP;
+
+  ace::GemmArgs g{};
+  g.act = at(L.xn);
+  g.perm = perm;
+  g.w0 = w->w_gate;
+  g.w1 = w->w_up;
+  g.out = at(L.H);
+  g.tile_expert = tile_e;
+  g.tile_row0 = tile_r0;
+  g.tile_rows = tile_rows;
+  g.n_tiles = n_tiles;
+  g.dense_rows = 0;
+  g.max_groups = L.max_groups;
+  g.d = d.d;
+  g.m = d.m;
+  if (ace::launch_gateup(g, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+
+  ace::GemmArgs gd = g;
+  gd.act = at(L.H);
+  gd.perm = nullptr;
+  gd.w0 = w->w_down;
+  gd.w1 = nullptr;
+  gd.out = at(L.Y);
+  if (ace::launch_down(gd, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+
+  const void *Ys = nullptr;
+  if (d.n_shared == 1) {
+    ace::GemmArgs s{};
+    s.act = at(L.xn);
+    s.perm = nullptr;
+    s.w0 = w->ws_gate;
+    s.w1 = w->ws_up;
+    s.out = at(L.Hs);
+    s.dense_rows = d.T;
+    s.max_groups = L.dense_groups;
+    s.d = d.d;
+    s.m = d.m_shared;
+    if (ace::launch_gateup(s, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+    ace::GemmArgs sd = s;
+    sd.act = at(L.Hs);
+    sd.w0 = w->ws_down;
+    sd.w1 = nullptr;
+    sd.out = at(L.Ys);
+    if (ace::launch_down(sd, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+    Ys = at(L.Ys);
+  }
+
+  ace::CombineArgs c{};
+  c.Y = at(L.Y);
+  c.Ys = Ys;
+  c.slot_row = slot_row;
+  c.gates = gates;
+  c.y = out->y;
+  c.T = d.T;
+  c.d = d.d;
+  c.k = d.k;
+  if (ace::launch_combine(c, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+  return ACE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,118 @@
+"""torch-facing wrapper of the ACE MoE layer forward.
+
+`moe_forward` marshals torch device tensors into the C ABI of libace.so and
+enqueues the layer on the current HIP stream.  torch provides device memory and
+the stream only; every step of the layer runs in the library's HIP kernels.
+"""
+from __future__ import annotations
+
+import torch
+
+from . import _lib
+
+_DT = {torch.bfloat16: _lib.ACE_BF16, torch.float32: _lib.ACE_F32}
+_WS_CACHE: dict = {}
+
+
+def _ptr(t):
+    return 0 if t is None else int(t.data_ptr())
+
+
+def _check(t, name, shape, dtype, device):
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)} != {tuple(shape)}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype} != {dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, expected {device}")
+
+
+def make_desc(T, d, N, k, m, dtype, tau, m_min=1, eps=1e-6, rms_eps=1e-6, n_shared=0, m_shared=0,
+              skip_disable=False, write_scores=False) -> _lib.Desc:
+    flags = (_lib.ACE_SKIP_DISABLE if skip_disable else 0) | (_lib.ACE_WRITE_SCORES if write_scores else 0)
+    dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
+    return _lib.Desc(T, d, N, k, m, n_shared, m_shared, dt, m_min, float(tau), float(eps),
+                     float(rms_eps), flags)
+
+
+def workspace(desc: _lib.Desc, device) -> torch.Tensor:
+    """A cached uint8 device buffer of ace_moe_workspace_size(desc) bytes."""
+    n = _lib.workspace_size(desc)
+    key = (str(device), torch.cuda.current_stream(device).cuda_stream)
+    buf = _WS_CACHE.get(key)
+    if buf is None or buf.numel() < n:
+        buf = torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+        _WS_CACHE[key] = buf
+    return buf
+
+
+def moe_forward(x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: int = 1,
+                eps: float = 1e-6, rms_eps: float = 1e-6, skip_disable: bool = False,
+                write_scores: bool = False, want_plan: bool = False, out: dict | None = None,
+                ws: torch.Tensor | None = None) -> dict:
+    """One ACE MoE layer forward on the GPU.
+
+    x        [T, d] bf16 or fp32 device tensor (the layer input before RMSNorm)
+    weights  dict: gamma [d], w_router [N, d], b_router [N] fp32 or None,
+             w_gate / w_up [N, m, d], w_down [N, d, m], and optionally
+             ws_gate / ws_up [m_s, d], ws_down [d, m_s] (one shared expert)
+    a_gsp, a_rcr  [N] fp32 amplification tables
+    Returns dict(y, topk_idx, keep, gates[, scores][, counts, offsets, perm]).
+    """
+    dev = x.device
+    T, d = x.shape
+    dtype = x.dtype
+    if dtype not in _DT:
+        raise ValueError(f"unsupported dtype {dtype}")
+    wg = weights["w_gate"]
+    N, m, _ = wg.shape
+    shared = weights.get("ws_gate") is not None
+    ms = weights["ws_gate"].shape[0] if shared else 0
+    _check(x, "x", (T, d), dtype, dev)
+    _check(weights["gamma"], "gamma", (d,), dtype, dev)
+    _check(weights["w_router"], "w_router", (N, d), dtype, dev)
+    if weights.get("b_router") is not None:
+        _check(weights["b_router"], "b_router", (N,), torch.float32, dev)
+    _check(wg, "w_gate", (N, m, d), dtype, dev)
+    _check(weights["w_up"], "w_up", (N, m, d), dtype, dev)
+    _check(weights["w_down"], "w_down", (N, d, m), dtype, dev)
+    if shared:
+        _check(weights["ws_gate"], "ws_gate", (ms, d), dtype, dev)
+        _check(weights["ws_up"], "ws_up", (ms, d), dtype, dev)
+        _check(weights["ws_down"], "ws_down", (d, ms), dtype, dev)
+    _check(a_gsp, "a_gsp", (N,), torch.float32, dev)
+    _check(a_rcr, "a_rcr", (N,), torch.float32, dev)
+
+    desc = make_desc(T, d, N, k, m, dtype, tau, m_min, eps, rms_eps, 1 if shared else 0, ms,
+                     skip_disable, write_scores)
+    if out is None:
+        out = {}
+    o = dict(out)
+    o.setdefault("y", torch.empty((T, d), dtype=dtype, device=dev))
+    o.setdefault("topk_idx", torch.empty((T, k), dtype=torch.int32, device=dev))
+    o.setdefault("keep", torch.empty((T, k), dtype=torch.uint8, device=dev))
+    o.setdefault("gates", torch.empty((T, k), dtype=torch.float32, device=dev))
+    if write_scores:
+        o.setdefault("scores", torch.empty((T, k), dtype=torch.float32, device=dev))
+    if want_plan:
+        o.setdefault("counts", torch.empty((N,), dtype=torch.int32, device=dev))
+        o.setdefault("offsets", torch.empty((N + 1,), dtype=torch.int32, device=dev))
+        o.setdefault("perm", torch.empty((max(T * k, 1),), dtype=torch.int32, device=dev))
+    W = _lib.Weights(_ptr(weights["gamma"]), _ptr(weights["w_router"]), _ptr(weights.get("b_router")),
+                     _ptr(wg), _ptr(weights["w_up"]), _ptr(weights["w_down"]),
+                     _ptr(weights.get("ws_gate")), _ptr(weights.get("ws_up")),
+                     _ptr(weights.get("ws_down")), _ptr(a_gsp), _ptr(a_rcr))
+    O = _lib.Outputs(_ptr(o["y"]), _ptr(o["topk_idx"]), _ptr(o["keep"]), _ptr(o.get("gates")),
+                     _ptr(o.get("scores")), _ptr(o.get("counts")), _ptr(o.get("offsets")),
+                     _ptr(o.get("perm")))
+    if ws is None:
+        ws = workspace(desc, dev)
+    stream = torch.cuda.current_stream(dev).cuda_stream
+    st = _lib.forward_raw(desc, _ptr(x), W, O, _ptr(ws), ws.numel(), stream)
+    if st != _lib.ACE_OK:
+        raise _lib.AceError(st, _lib.status_string(st))
+    return o

@@ -1,9 +1,10 @@
 """Seeded generators for the ACE MoE layer inputs.
 
-Every tensor comes from its own stream
-``PCG64(SeedSequence([seed, layer, tensor_id]))``: values are drawn in fp64,
-scaled, then rounded to the storage dtype (fp32, or fp32 then bf16 with
-round-to-nearest-even).  The arrays returned are float32 arrays whose values
+Every tensor is cut into blocks along its first axis (one expert of a weight
+stack, or 256 rows of a matrix), and block c comes from its own stream
+``PCG64(SeedSequence([seed, layer, tensor_id, c]))``, so blocks can be drawn in
+parallel.  Values are drawn in fp64, scaled, then rounded to the storage dtype
+(fp32, or fp32 then bf16 with round-to-nearest-even).  The arrays returned are float32 arrays whose values
 are exactly representable in the storage dtype, so the GPU and the oracle see
 the same numbers.
 
@@ -11,6 +12,9 @@ Tensor ids: x=0, gamma=1, router=2, gate=3, up=4, down=5, Zipf permutation=6,
 shared gate/up/down=7/8/9, decode step s = 100+s.
 """
 from __future__ import annotations
+
+import os
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -21,8 +25,17 @@ TID_ZIPF, TID_SGATE, TID_SUP, TID_SDOWN = 6, 7, 8, 9
 TID_DECODE0 = 100
 
 
-def rng_for(seed: int, layer: int, tensor_id: int) -> np.random.Generator:
-    return np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, layer, tensor_id])))
+def rng_for(seed: int, layer: int, tensor_id: int, block: int | None = None) -> np.random.Generator:
+    key = [seed, layer, tensor_id] if block is None else [seed, layer, tensor_id, block]
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(key)))
+
+
+def _workers() -> int:
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
 
 
 def f32_to_bf16_bits(a) -> np.ndarray:
@@ -50,23 +63,24 @@ def _to_dtype(a64: np.ndarray, dtype: str) -> np.ndarray:
     raise ValueError(f"unknown dtype {dtype!r}")
 
 
-def _normal(cfg: LayerConfig, layer: int, tid: int, shape, std: float, mean: float = 0.0,
-            chunk_rows: int | None = None) -> np.ndarray:
-    """N(mean, std) draws of `shape`, produced row-block by row-block along axis 0.
-
-    Drawing in blocks from one generator gives the same stream as a single draw,
-    so the result does not depend on the block size (only memory use does).
-    """
-    g = rng_for(cfg.seed, layer, tid)
+def _normal(cfg: LayerConfig, layer: int, tid: int, shape, std: float, mean: float = 0.0) -> np.ndarray:
+    """N(mean, std) draws of `shape`, block by block along axis 0 (see module doc)."""
+    shape = tuple(shape)
     out = np.empty(shape, dtype=np.float32)
     rows = shape[0]
-    per_row = int(np.prod(shape[1:])) if len(shape) > 1 else 1
-    if chunk_rows is None:
-        chunk_rows = max(1, (1 << 21) // max(per_row, 1))
-    for r0 in range(0, rows, chunk_rows):
-        r1 = min(rows, r0 + chunk_rows)
-        blk = g.standard_normal((r1 - r0,) + tuple(shape[1:]))
-        out[r0:r1] = _to_dtype(mean + std * blk, cfg.dtype)
+    step = 1 if len(shape) == 3 else 256
+    blocks = [(c, r0, min(rows, r0 + step)) for c, r0 in enumerate(range(0, rows, step))]
+
+    def fill(blk):
+        c, r0, r1 = blk
+        g = rng_for(cfg.seed, layer, tid, c)
+        out[r0:r1] = _to_dtype(mean + std * g.standard_normal((r1 - r0,) + shape[1:]), cfg.dtype)
+
+    if len(blocks) == 1:
+        fill(blocks[0])
+    else:
+        with ThreadPoolExecutor(max_workers=_workers()) as ex:
+            list(ex.map(fill, blocks))
     return out
 
 
