@@ -1,0 +1,246 @@
+#!/usr/bin/env python3
+"""Benchmark of the ACE token-adaptive MoE layer forward on one MI355X.
+
+Workload: one bf16 MoE layer shaped like a 30B-total / 3B-active model
+(hidden 2048, 128 experts, top-8, expert intermediate 768), 4096-token prefill
+at a 50% skip ratio, with seeded synthetic inputs (activations N(0,1), RMSNorm
+gamma 1+N(0,0.1), weights N(0,0.02)).  The GSP/RCR tables and tau are the
+oracle-built values stored in tests/golden/ (inputs of the layer, like weights).
+
+One step = one full layer forward (RMSNorm, router, top-k, ACE skip mask,
+dispatch plan, grouped gate/up + SwiGLU, grouped down, combine) on inputs
+already resident in HBM.  Prints ONE JSON line.  Besides `value` (prefill
+tokens/s) it reports the speedup over the plain top-k layer through the same
+kernels, decode batches 1/8/32/64 (tau transferred from prefill), per-stage
+times from HIP events recorded on the layer's stream, the roofline of the
+dominant kernel and the CPU oracle timed on a bounded token sample.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--prefill-only] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
+METRIC = "MoE-layer tokens/s at 50% skip (prefill, decode); speedup vs plain top-k"
+TABLES = os.path.join(ROOT, "tests", "golden", "tables_prefill_4096_seed0.json")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--q", default="0.5", help="skip ratio whose stored tau is used")
+    ap.add_argument("--prefill-only", action="store_true", help="time only the ACE prefill step")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle sample budget")
+    return ap.parse_args()
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def time_steps(fn, steps: int, warmup: int, torch) -> float:
+    """ms per step over `steps` timed calls after `warmup` untimed ones."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        fn()
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3 / steps
+
+
+def stage_profile(fn, steps: int, ace, torch) -> dict:
+    """Average ms per stage over `steps` calls, from HIP events the library
+    records on the layer's stream around each stage."""
+    torch.cuda.synchronize()
+    ace.profile_begin(steps)
+    try:
+        for _ in range(steps):
+            fn()
+    finally:
+        tot, n = ace.profile_end()
+    return {k: v / max(n, 1) for k, v in tot.items()}
+
+
+def layer_bytes(T, d, N, k, m, e_act, n_kept, esz=2):
+    """Algorithmic HBM bytes of one layer forward and of each stage."""
+    w_exp = 3 * m * d * esz
+    st = {
+        "route": 2 * T * d * esz + N * d * esz + d * esz + T * k * 13,
+        "plan": N * ((T + 63) // 64) * 8 + T * k * 8 + N * 8,
+        "gateup": e_act * 2 * m * d * esz + T * d * esz + n_kept * m * esz,
+        "down": e_act * m * d * esz + n_kept * m * esz + n_kept * d * esz,
+        "combine": n_kept * d * esz + T * d * esz + T * k * 8,
+    }
+    total = e_act * w_exp + N * d * esz + 2 * T * d * esz + T * k * 13
+    return total, st
+
+
+def cpu_baseline(L, k, a_gsp, a_rcr, tau, budget_s):
+    """The oracle's online forward (as it stands) on the first n tokens of the
+    same input, n sized for about `budget_s` seconds of CPU work."""
+    import numpy as np
+
+    import oracle  # the CPU oracle: used only for this baseline leg
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        cores = 1
+
+    def run(n):
+        Ls = dict(L, x=L["x"][:n], cfg=L["cfg"].with_(T=n))
+        t0 = time.perf_counter()
+        oracle.forward.moe_forward(Ls, k, a_gsp, a_rcr, float(np.float32(tau)))
+        return time.perf_counter() - t0
+
+    t8 = run(8)
+    n = int(max(8, min(L["cfg"].T, 8 * budget_s / max(t8, 1e-3))))
+    t = run(n)
+    return {"value": n / t, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {n} of the 4096 prefill tokens, full online forward in fp64 numpy "
+                      f"({t:.1f} s)"}
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU only: the ACE layer here has no multi-GPU path "
+              "(token sharding needs no exchange; see DESIGN.md). Use --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_05228_amd as ace
+    import synth
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    ace.lib()  # fail loudly if the HIP library is missing
+    dev = "cuda:0"
+    gold = json.load(open(TABLES))
+    cfg = synth.config("prefill_4096")
+    assert gold["config"]["T"] == cfg.T and gold["config"]["seed"] == cfg.seed
+    T, d, N, k, m = cfg.T, cfg.d, cfg.N, cfg.k, cfg.m
+    tau = float(gold["tau_f32"][args.q])
+    t0 = time.time()
+    L = synth.make_layer(cfg)
+    log(f"generated layer in {time.time() - t0:.1f}s; tau={tau}")
+    bf = torch.bfloat16
+    D = {key: torch.from_numpy(L[key]).to(dev).to(bf).contiguous()
+         for key in ("x", "gamma", "w_router", "w_gate", "w_up", "w_down")}
+    D["b_router"] = None
+    ag = torch.tensor(gold["a_gsp"], dtype=torch.float32, device=dev)
+    ar = torch.tensor(gold["a_rcr"], dtype=torch.float32, device=dev)
+
+    def make_step(x, skip_disable, tau_):
+        desc = ace.make_desc(x.shape[0], d, N, k, m, bf, tau_, skip_disable=skip_disable)
+        ws = torch.empty(ace.workspace_size(desc), dtype=torch.uint8, device=dev)
+        out = {"y": torch.empty_like(x), "topk_idx": torch.empty((x.shape[0], k), dtype=torch.int32, device=dev),
+               "keep": torch.empty((x.shape[0], k), dtype=torch.uint8, device=dev),
+               "gates": torch.empty((x.shape[0], k), dtype=torch.float32, device=dev),
+               "counts": torch.empty((N,), dtype=torch.int32, device=dev),
+               "offsets": torch.empty((N + 1,), dtype=torch.int32, device=dev),
+               "perm": torch.empty((x.shape[0] * k,), dtype=torch.int32, device=dev)}
+
+        def fn():
+            return ace.moe_forward(x, D, ag, ar, k=k, tau=tau_, skip_disable=skip_disable, out=out, ws=ws,
+                                   want_plan=True)
+        return fn, out
+
+    # ---------------- prefill, ACE at the requested skip ratio
+    ace_step, ace_out = make_step(D["x"], False, tau)
+    log(f"timing prefill: {args.warmup} warmup + {args.steps} steps")
+    ms = time_steps(ace_step, args.steps, args.warmup, torch)
+    keep = ace_out["keep"].cpu().numpy()
+    counts = ace_out["counts"].cpu().numpy()
+    n_kept = int(keep.sum())
+    e_act = int((counts > 0).sum())
+    realised = 1.0 - n_kept / keep.size
+    stages = stage_profile(ace_step, args.steps, ace, torch)
+    log(f"prefill {ms:.3f} ms/step, skip {realised:.4f}, E_act {e_act}, stages {stages}")
+
+    total_b, st_b = layer_bytes(T, d, N, k, m, e_act, n_kept)
+    flops_mfma = 6 * d * m * n_kept
+    dom = max(("route", "plan", "gateup", "down", "combine"), key=lambda s: stages[s])
+    dom_ms = stages[dom]
+    achieved = st_b[dom] / (dom_ms * 1e-3) / 1e9
+    roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "avg_launch_ms": round(dom_ms, 5), "alg_bytes_per_launch": int(st_b[dom])}
+    if dom in ("gateup", "down"):
+        f = 4 * d * m * n_kept if dom == "gateup" else 2 * d * m * n_kept
+        roofline["mfma_tflops"] = round(f / (dom_ms * 1e-3) / 1e12, 1)
+        roofline["mfma_frac"] = round(f / (dom_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4)
+    t_lb = max(flops_mfma / (BF16_PEAK_TFLOPS * 1e12), total_b / (HBM_PEAK_GBS * 1e9))
+    layer_roof = {"alg_bytes": int(total_b), "mfma_flop": int(flops_mfma),
+                  "bound": "hbm" if total_b / (HBM_PEAK_GBS * 1e9) >= flops_mfma / (BF16_PEAK_TFLOPS * 1e12)
+                  else "mfma",
+                  "t_lower_bound_ms": round(t_lb * 1e3, 4), "frac": round(t_lb * 1e3 / ms, 4),
+                  "hbm_gbs": round(total_b / (ms * 1e-3) / 1e9, 1),
+                  "mfma_tflops": round(flops_mfma / (ms * 1e-3) / 1e12, 1)}
+
+    result = {
+        "metric": METRIC, "value": round(T / (ms * 1e-3), 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "prefill_4096: one bf16 MoE layer, T=4096 d=2048 N=128 top-8 m=768, "
+                               "ACE skip target 0.5 (seeded synthetic inputs)",
+                   "T": T, "d": d, "N": N, "k": k, "m": m, "skip_target": float(args.q), "tau": tau,
+                   "realised_skip": round(realised, 5), "experts_active": e_act, "kept_slots": n_kept},
+        "stages_ms": {s: round(v, 5) for s, v in stages.items()},
+        "roofline": roofline,
+        "layer_roofline": layer_roof,
+    }
+
+    if not args.prefill_only:
+        # ---------------- plain top-k through the same kernels (speedup baseline)
+        top_step, _ = make_step(D["x"], True, tau)
+        ms_top = time_steps(top_step, args.steps, args.warmup, torch)
+        result["topk_ms_per_step"] = round(ms_top, 4)
+        result["speedup_vs_topk"] = round(ms_top / ms, 4)
+        log(f"plain top-k {ms_top:.3f} ms/step -> speedup {ms_top / ms:.3f}")
+
+        # ---------------- decode batches, tau transferred from prefill
+        dec = {}
+        for B in (1, 8, 32, 64):
+            xb = torch.from_numpy(synth.decode_inputs(cfg.with_(T=B), B, step=0)).to(dev).to(bf)
+            s_ace, o_ace = make_step(xb, False, tau)
+            s_top, _ = make_step(xb, True, tau)
+            ms_a = time_steps(s_ace, max(args.steps, 50), args.warmup, torch)
+            ms_t = time_steps(s_top, max(args.steps, 50), args.warmup, torch)
+            kb = o_ace["keep"].cpu().numpy()
+            ea = int((o_ace["counts"].cpu().numpy() > 0).sum())
+            bb, _ = layer_bytes(B, d, N, k, m, ea, int(kb.sum()))
+            dec[str(B)] = {"tokens_per_s": round(B / (ms_a * 1e-3), 1), "ms_per_step": round(ms_a, 4),
+                           "topk_ms_per_step": round(ms_t, 4), "speedup_vs_topk": round(ms_t / ms_a, 4),
+                           "realised_skip": round(1 - kb.mean(), 4), "experts_active": ea,
+                           "alg_gbs": round(bb / (ms_a * 1e-3) / 1e9, 1),
+                           "hbm_frac": round(bb / (ms_a * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            log(f"decode B={B}: {dec[str(B)]}")
+        result["decode"] = dec
+
+    if not args.no_cpu and not args.prefill_only:
+        log("timing the CPU oracle on a token sample")
+        result["cpu_baseline"] = cpu_baseline(L, k, np.array(gold["a_gsp"], np.float32),
+                                              np.array(gold["a_rcr"], np.float32), tau, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

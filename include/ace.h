@@ -122,6 +122,26 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
                            const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
                            void *stream);
 
+/*
+ * Stage timing, for measurement only (computing the layer never needs it).
+ * ace_profile_begin(max_calls) creates max_calls x (ACE_PROFILE_STAGES + 1) HIP
+ * events on the current device; each following ace_moe_forward (up to max_calls)
+ * records one set on its own stream: before the first stage and after each stage
+ *   0 route  (bitmap clear; RMSNorm, router, top-k, Alg. 4 skip mask)
+ *   1 plan   (histogram, prefix sum, permutation, M tiles)
+ *   2 gateup (grouped gate/up GEMM with the SwiGLU epilogue)
+ *   3 down   (grouped down GEMM)
+ *   4 shared (dense shared expert; empty when n_shared = 0)
+ *   5 combine.
+ * ace_profile_end waits for the recorded events, writes the per-stage elapsed
+ * time summed over the recorded calls (ms) into stage_ms[0..n_stages-1] and the
+ * number of recorded calls into *n_calls, and destroys the events.  Only one
+ * profile may be open per process; begin while open -> ACE_ERR_INVALID_ARG.
+ */
+#define ACE_PROFILE_STAGES 6
+ace_status ace_profile_begin(int max_calls);
+ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls);
+
 /* Static, human-readable text of a status code (never NULL). */
 const char *ace_status_string(int status);
 

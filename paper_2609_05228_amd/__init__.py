@@ -8,7 +8,7 @@ layer on the current HIP stream.
 """
 from ._lib import (  # noqa: F401
     ACE_BF16, ACE_ERR_HIP, ACE_ERR_INVALID_ARG, ACE_ERR_UNSUPPORTED, ACE_ERR_WORKSPACE, ACE_F32,
-    ACE_OK, ACE_SKIP_DISABLE, ACE_WRITE_SCORES, AceError, Desc, LIB_PATH, Outputs, Weights,
-    abi_version, forward_raw, lib, status_string, workspace_size,
+    ACE_OK, ACE_SKIP_DISABLE, ACE_WRITE_SCORES, PROFILE_STAGES, AceError, Desc, LIB_PATH, Outputs,
+    Weights, abi_version, forward_raw, lib, profile_begin, profile_end, status_string, workspace_size,
 )
 from .layer import make_desc, moe_forward, workspace  # noqa: F401

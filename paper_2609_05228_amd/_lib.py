@@ -71,6 +71,11 @@ def lib() -> ctypes.CDLL:
         L.ace_status_string.restype = ctypes.c_char_p
         L.ace_abi_version.argtypes = []
         L.ace_abi_version.restype = ctypes.c_int
+        L.ace_profile_begin.argtypes = [ctypes.c_int]
+        L.ace_profile_begin.restype = ctypes.c_int
+        L.ace_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int,
+                                      ctypes.POINTER(ctypes.c_int)]
+        L.ace_profile_end.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -81,6 +86,25 @@ def status_string(status: int) -> str:
 
 def abi_version() -> int:
     return int(lib().ace_abi_version())
+
+
+PROFILE_STAGES = ("route", "plan", "gateup", "down", "shared", "combine")
+
+
+def profile_begin(max_calls: int) -> None:
+    st = int(lib().ace_profile_begin(int(max_calls)))
+    if st != ACE_OK:
+        raise AceError(st, status_string(st))
+
+
+def profile_end() -> tuple[dict, int]:
+    """(summed ms per stage over the recorded calls, number of recorded calls)."""
+    arr = (ctypes.c_double * len(PROFILE_STAGES))()
+    n = ctypes.c_int(0)
+    st = int(lib().ace_profile_end(arr, len(PROFILE_STAGES), ctypes.byref(n)))
+    if st != ACE_OK:
+        raise AceError(st, status_string(st))
+    return dict(zip(PROFILE_STAGES, list(arr))), int(n.value)
 
 
 def workspace_size(desc: Desc) -> int:

@@ -9,6 +9,8 @@
 
 #include <cmath>
 #include <cstdint>
+#include <mutex>
+#include <vector>
 
 #include "../../include/ace.h"
 #include "ace_internal.h"
@@ -96,9 +98,80 @@ ace_status validate(const ace_moe_desc *d, const void *x, const ace_moe_weights 
   return ACE_OK;
 }
 
+// ---------------------------------------------------------------- stage timing
+// Measurement hook only: while a profile is open, every forward records
+// ACE_PROFILE_STAGES + 1 events on its stream (before the first stage and after
+// each stage), one set per call, up to the capacity given at begin.
+struct Profile {
+  std::mutex mu;
+  bool on = false;
+  int cap = 0;
+  int used = 0;
+  std::vector<hipEvent_t> ev;  // cap x (stages + 1)
+};
+Profile g_prof;
+constexpr int kStages = ACE_PROFILE_STAGES;
+
+// events of the next call, or null when no profile is open (or it is full)
+hipEvent_t *profile_slot() {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on || g_prof.used >= g_prof.cap) return nullptr;
+  return &g_prof.ev[static_cast<size_t>(g_prof.used++) * (kStages + 1)];
+}
+
+void mark(hipEvent_t *slot, int i, hipStream_t s) {
+  if (slot) (void)hipEventRecord(slot[i], s);
+}
+
 }  // namespace
 
 extern "C" {
+
+ace_status ace_profile_begin(int max_calls) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (g_prof.on || max_calls <= 0 || max_calls > 100000) return ACE_ERR_INVALID_ARG;
+  g_prof.ev.assign(static_cast<size_t>(max_calls) * (kStages + 1), nullptr);
+  for (auto &e : g_prof.ev)
+    if (hipEventCreate(&e) != hipSuccess) {
+      for (auto &x : g_prof.ev)
+        if (x) (void)hipEventDestroy(x);
+      g_prof.ev.clear();
+      return ACE_ERR_HIP;
+    }
+  g_prof.cap = max_calls;
+  g_prof.used = 0;
+  g_prof.on = true;
+  return ACE_OK;
+}
+
+ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls) {
+  std::lock_guard<std::mutex> lk(g_prof.mu);
+  if (!g_prof.on) return ACE_ERR_INVALID_ARG;
+  ace_status st = ACE_OK;
+  for (int j = 0; j < n_stages && stage_ms; ++j) stage_ms[j] = 0.0;
+  for (int c = 0; c < g_prof.used && st == ACE_OK; ++c) {
+    hipEvent_t *e = &g_prof.ev[static_cast<size_t>(c) * (kStages + 1)];
+    if (hipEventSynchronize(e[kStages]) != hipSuccess) {
+      st = ACE_ERR_HIP;
+      break;
+    }
+    for (int j = 0; j < kStages && j < n_stages; ++j) {
+      float ms = 0.f;
+      if (hipEventElapsedTime(&ms, e[j], e[j + 1]) != hipSuccess) {
+        st = ACE_ERR_HIP;
+        break;
+      }
+      if (stage_ms) stage_ms[j] += ms;
+    }
+  }
+  if (n_calls) *n_calls = g_prof.used;
+  for (auto &x : g_prof.ev) (void)hipEventDestroy(x);
+  g_prof.ev.clear();
+  g_prof.on = false;
+  g_prof.cap = g_prof.used = 0;
+  return st;
+}
+
 
 size_t ace_moe_workspace_size(const ace_moe_desc *desc) {
   if (!desc || desc->T <= 0 || desc->d <= 0 || desc->N <= 0 || desc->k <= 0 || desc->m <= 0) return 0;
@@ -145,6 +218,8 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   auto *tile_rows = static_cast<int32_t *>(at(L.tile_rows));
   auto *n_tiles = static_cast<int32_t *>(at(L.n_tiles));
 
+  hipEvent_t *prof = profile_slot();
+  mark(prof, 0, stream);
   hipError_t e = ace::launch_zero_u64(bitmap, static_cast<size_t>(d.N) * L.W, stream);
   if (e != hipSuccess) return ACE_ERR_HIP;
 
@@ -173,6 +248,7 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   ra.rms_eps = d.rms_eps;
   ra.skip_disable = (d.flags & ACE_SKIP_DISABLE) ? 1 : 0;
   if (ace::launch_route(ra, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+  mark(prof, 1, stream);
 
   ace::PlanArgs pa{};
   pa.bitmap = bitmap;
@@ -190,6 +266,7 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   pa.N = d.N;
   pa.W = L.W;
   if (ace::launch_plan(pa, stream) != hipSuccess) return ACE_ERR_HIP;
+  mark(prof, 2, stream);
 
   ace::GemmArgs g{};
   g.act = at(L.xn);
@@ -206,6 +283,7 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   g.d = d.d;
   g.m = d.m;
   if (ace::launch_gateup(g, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+  mark(prof, 3, stream);
 
   ace::GemmArgs gd = g;
   gd.act = at(L.H);
@@ -214,6 +292,7 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   gd.w1 = nullptr;
   gd.out = at(L.Y);
   if (ace::launch_down(gd, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+  mark(prof, 4, stream);
 
   const void *Ys = nullptr;
   if (d.n_shared == 1) {
@@ -236,6 +315,7 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
     if (ace::launch_down(sd, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
     Ys = at(L.Ys);
   }
+  mark(prof, 5, stream);
 
   ace::CombineArgs c{};
   c.Y = at(L.Y);
@@ -247,6 +327,7 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   c.d = d.d;
   c.k = d.k;
   if (ace::launch_combine(c, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+  mark(prof, 6, stream);
   return ACE_OK;
 }
 
