@@ -127,8 +127,8 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
  * ace_profile_begin(max_calls) creates max_calls x (ACE_PROFILE_STAGES + 1) HIP
  * events on the current device; each following ace_moe_forward (up to max_calls)
  * records one set on its own stream: before the first stage and after each stage
- *   0 route  (bitmap clear; RMSNorm, router, top-k, Alg. 4 skip mask)
- *   1 plan   (histogram, prefix sum, permutation, M tiles)
+ *   0 route  (RMSNorm, router, top-k, Alg. 4 skip mask, per-chunk expert counts)
+ *   1 plan   (expert histogram and prefix sums, permutation, M tiles)
  *   2 gateup (grouped gate/up GEMM with the SwiGLU epilogue)
  *   3 down   (grouped down GEMM)
  *   4 shared (dense shared expert; empty when n_shared = 0)

@@ -37,7 +37,8 @@ template <> struct Elem<bf16_t> {
 
 constexpr int kMaxN = 256;   // routed experts supported by the router kernel
 constexpr int kMaxK = 8;     // top-k supported by the router kernel
-constexpr int kTileM = 128;  // rows of one grouped-GEMM M tile (the dispatch plan's tile size)
+constexpr int kTileM = 256;  // rows of one grouped-GEMM M tile (the dispatch plan's tile size)
+constexpr int kRouteTokens = 16;  // tokens per router workgroup (one dispatch-plan chunk)
 
 // ---------------------------------------------------------------- kernel arguments
 struct RouteArgs {
@@ -53,15 +54,19 @@ struct RouteArgs {
   float *gates;           // [T, k] ghat
   float *scores;          // [T, k] c, or null
   int32_t *slot_row;      // [T, k]: -1 for skipped slots (kept slots are filled by the plan)
-  unsigned long long *bitmap;  // [N, W] token bitmap of kept (expert, token) pairs
-  int T, d, N, k, m_min, W;
+  uint8_t *local_rank;    // [T, k]: rank of a kept slot among its chunk's kept slots of that expert
+  uint8_t *chunk_count;   // [G, N]: kept slots per (16-token chunk, expert)
+  int T, d, N, k, m_min;
   float tau, eps, rms_eps;
   int skip_disable;
 };
 
 struct PlanArgs {
-  const unsigned long long *bitmap;  // [N, W]
+  const uint8_t *chunk_count;        // [G, N]
+  const uint8_t *local_rank;         // [T, k]
   const int32_t *topk_idx;           // [T, k]
+  const uint8_t *keep;               // [T, k]
+  int32_t *chunk_base;               // [N, G]: kept slots of expert e in chunks before g
   int32_t *counts;                   // [N]
   int32_t *offsets;                  // [N+1]
   int32_t *perm;                     // [T*k]
@@ -70,7 +75,7 @@ struct PlanArgs {
   int32_t *tile_row0;                // [max_tiles]
   int32_t *tile_rows;                // [max_tiles]
   int32_t *n_tiles;                  // [1]
-  int T, k, N, W;
+  int T, k, N, G;
 };
 
 // Grouped GEMM over the dispatch plan.  Tile g covers rows tile_row0[g] ..
@@ -100,7 +105,6 @@ struct CombineArgs {
 
 // ---------------------------------------------------------------- launchers
 // Each returns hipGetLastError() after enqueueing on `stream`.
-hipError_t launch_zero_u64(unsigned long long *p, size_t n, hipStream_t stream);
 hipError_t launch_route(const RouteArgs &a, bool bf16, hipStream_t stream);
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);
 hipError_t launch_gateup(const GemmArgs &a, bool bf16, hipStream_t stream);

@@ -1,7 +1,7 @@
 // C ABI of the ACE MoE layer: host-side validation, workspace layout and the
 // launch sequence of one layer forward (Alg. 1's online loop for one layer):
-//   zero bitmap -> route (RMSNorm, router, top-k, Alg. 4 skip mask)
-//   -> plan (histogram, prefix sum, permutation, M tiles)
+//   route (RMSNorm, router, top-k, Alg. 4 skip mask, per-chunk expert counts)
+//   -> plan (expert scan, then prefix sum, permutation and M tiles)
 //   -> grouped gate/up + SwiGLU -> grouped down
 //   -> [shared expert: dense gate/up -> dense down] -> gate-weighted combine.
 // Everything is enqueued on the caller's stream; nothing is allocated.
@@ -22,9 +22,9 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  size_t xn, bitmap, slot_row, gates, counts, offsets, perm, tile_e, tile_r0, tile_rows, n_tiles;
-  size_t H, Y, Hs, Ys, total;
-  int W, max_groups, dense_groups;
+  size_t xn, local_rank, chunk_count, chunk_base, slot_row, gates, counts, offsets, perm;
+  size_t tile_e, tile_r0, tile_rows, n_tiles, H, Y, Hs, Ys, total;
+  int G, max_groups, dense_groups;
 };
 
 Layout layout_for(const ace_moe_desc &d) {
@@ -33,7 +33,7 @@ Layout layout_for(const ace_moe_desc &d) {
   const size_t N = static_cast<size_t>(d.N), k = static_cast<size_t>(d.k), m = static_cast<size_t>(d.m);
   const size_t esz = (d.dtype == ACE_BF16) ? 2 : 4;
   const size_t slots = T * k;
-  L.W = static_cast<int>((T + 63) / 64);
+  L.G = static_cast<int>((T + ace::kRouteTokens - 1) / ace::kRouteTokens);
   L.max_groups = static_cast<int>((slots + ace::kTileM - 1) / ace::kTileM + (slots < N ? slots : N));
   L.dense_groups = static_cast<int>((T + ace::kTileM - 1) / ace::kTileM);
   size_t off = 0;
@@ -43,7 +43,9 @@ Layout layout_for(const ace_moe_desc &d) {
     return o;
   };
   L.xn = take(T * dd * esz);
-  L.bitmap = take(N * static_cast<size_t>(L.W) * 8);
+  L.local_rank = take(slots);
+  L.chunk_count = take(static_cast<size_t>(L.G) * N);
+  L.chunk_base = take(static_cast<size_t>(L.G) * N * 4);
   L.slot_row = take(slots * 4);
   L.gates = take(slots * 4);
   L.counts = take(N * 4);
@@ -207,7 +209,9 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   const bool bf16 = d.dtype == ACE_BF16;
   auto at = [&](size_t off) { return static_cast<void *>(ws + off); };
 
-  auto *bitmap = static_cast<unsigned long long *>(at(L.bitmap));
+  auto *local_rank = static_cast<uint8_t *>(at(L.local_rank));
+  auto *chunk_count = static_cast<uint8_t *>(at(L.chunk_count));
+  auto *chunk_base = static_cast<int32_t *>(at(L.chunk_base));
   auto *slot_row = static_cast<int32_t *>(at(L.slot_row));
   float *gates = out->gates ? out->gates : static_cast<float *>(at(L.gates));
   int32_t *counts = out->expert_counts ? out->expert_counts : static_cast<int32_t *>(at(L.counts));
@@ -220,8 +224,6 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
 
   hipEvent_t *prof = profile_slot();
   mark(prof, 0, stream);
-  hipError_t e = ace::launch_zero_u64(bitmap, static_cast<size_t>(d.N) * L.W, stream);
-  if (e != hipSuccess) return ACE_ERR_HIP;
 
   ace::RouteArgs ra{};
   ra.x = x;
@@ -236,13 +238,13 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   ra.gates = gates;
   ra.scores = (d.flags & ACE_WRITE_SCORES) ? out->scores : nullptr;
   ra.slot_row = slot_row;
-  ra.bitmap = bitmap;
+  ra.local_rank = local_rank;
+  ra.chunk_count = chunk_count;
   ra.T = d.T;
   ra.d = d.d;
   ra.N = d.N;
   ra.k = d.k;
   ra.m_min = d.m_min;
-  ra.W = L.W;
   ra.tau = d.tau;
   ra.eps = d.eps;
   ra.rms_eps = d.rms_eps;
@@ -251,8 +253,11 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   mark(prof, 1, stream);
 
   ace::PlanArgs pa{};
-  pa.bitmap = bitmap;
+  pa.chunk_count = chunk_count;
+  pa.local_rank = local_rank;
   pa.topk_idx = out->topk_idx;
+  pa.keep = out->keep;
+  pa.chunk_base = chunk_base;
   pa.counts = counts;
   pa.offsets = offsets;
   pa.perm = perm;
@@ -264,7 +269,7 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   pa.T = d.T;
   pa.k = d.k;
   pa.N = d.N;
-  pa.W = L.W;
+  pa.G = L.G;
   if (ace::launch_plan(pa, stream) != hipSuccess) return ACE_ERR_HIP;
   mark(prof, 2, stream);
 

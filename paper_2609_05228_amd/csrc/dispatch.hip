@@ -2,18 +2,18 @@
 // permutation of kept slots, plus the M-tile list the grouped GEMMs walk.
 //
 // The layer evaluates only the experts indexed by each token's active set
-// (Alg. 1's online loop).  The router kernel leaves one bit per kept
-// (expert, token) pair in a per-expert token bitmap; here one workgroup of 1024
-// threads turns the bitmap into
-//   counts[e]   = popcount of expert e's bitmap,
-//   offsets[e]  = exclusive prefix sum of counts,
-//   perm[r]     = token of compacted row r, rows ordered by (expert, token),
-//   slot_row    = compacted row of every kept (token, slot),
-//   tiles       = (expert, first row, rows) of every kTileM-row M tile.
-// The order is fixed by the bitmap, so the plan is bit-exact and independent
-// of how the router workgroups were scheduled.  P = 1024 / N threads share an
-// expert, each owning a contiguous run of bitmap words: pass 1 counts, a
-// wavefront scan over experts places them, pass 2 writes rows in token order.
+// (Alg. 1's online loop).  Compacted rows are ordered by (expert, token).  The
+// router kernel leaves, per 16-token chunk g and expert e, the kept count
+// chunk_count[g][e] and, per kept slot, its rank among the chunk's kept slots
+// of that expert.  Two kernels finish the plan:
+//   expert_scan (one workgroup per expert): chunk_base[e][g] = sum of
+//     chunk_count[g'][e] over g' < g, and counts[e];
+//   scatter (one workgroup per chunk): offsets = exclusive prefix sum of counts
+//     (each workgroup recomputes it; N <= 256), then every kept slot writes
+//     row = offsets[e] + chunk_base[e][g] + local_rank into perm and slot_row.
+//     Workgroup 0 also writes offsets and the M-tile list.
+// Integer work only, no atomics: the plan is bit-exact and independent of
+// scheduling.
 #include "ace_internal.h"
 
 namespace ace {
@@ -29,97 +29,102 @@ __device__ __forceinline__ int wave_inclusive_scan(int v, int lane) {
   return v;
 }
 
-__global__ __launch_bounds__(1024) void plan_kernel(PlanArgs a) {
-  __shared__ int cnt[1024];
-  __shared__ int ecount[kMaxN];
-  __shared__ int eoff[kMaxN + 1];
-  __shared__ int tcount[kMaxN];
-  __shared__ int toff[kMaxN + 1];
+// exclusive scan of v[0..n) (n <= 256) by one wavefront into out[0..n]
+__device__ __forceinline__ void wave_scan_256(const int *v, int *out, int n, int lane) {
+  int loc[4];
+  int s = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = lane * 4 + j;
+    loc[j] = s;
+    s += (i < n) ? v[i] : 0;
+  }
+  const int incl = wave_inclusive_scan(s, lane);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int i = lane * 4 + j;
+    if (i < n) out[i] = incl - s + loc[j];
+  }
+  if (lane == 63) out[n] = incl;
+}
 
+__global__ __launch_bounds__(256) void expert_scan_kernel(PlanArgs a) {
+  __shared__ int part[256];
+  const int e = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int G = a.G, N = a.N;
+  const int per = (G + 255) / 256;
+  const int g0 = min(G, tid * per), g1 = min(G, g0 + per);
+  int s = 0;
+  for (int g = g0; g < g1; ++g) s += a.chunk_count[static_cast<size_t>(g) * N + e];
+  part[tid] = s;
+  __syncthreads();
+  if (tid < 64) {
+    // exclusive scan of the 256 partial sums
+    int loc[4];
+    int acc = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      loc[j] = acc;
+      acc += part[tid * 4 + j];
+    }
+    const int incl = wave_inclusive_scan(acc, tid);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) part[tid * 4 + j] = incl - acc + loc[j];
+    if (tid == 63) a.counts[e] = incl;
+  }
+  __syncthreads();
+  int run = part[tid];
+  int32_t *base = a.chunk_base + static_cast<size_t>(e) * G;
+  for (int g = g0; g < g1; ++g) {
+    base[g] = run;
+    run += a.chunk_count[static_cast<size_t>(g) * N + e];
+  }
+}
+
+__global__ __launch_bounds__(128) void scatter_kernel(PlanArgs a) {
+  __shared__ int cnt[kMaxN];
+  __shared__ int off[kMaxN + 1];
+  __shared__ int tcnt[kMaxN];
+  __shared__ int toff[kMaxN + 1];
   const int tid = threadIdx.x;
   const int N = a.N;
-  const int W = a.W;
-  const int P = 1024 / N;
-  const int e = tid / P;
-  const int p = tid - e * P;
-  const bool active = e < N;
-  const int cw = (W + P - 1) / P;
-  const int w0 = active ? min(W, p * cw) : 0;
-  const int w1 = active ? min(W, w0 + cw) : 0;
-  const unsigned long long *bm = a.bitmap + static_cast<size_t>(active ? e : 0) * W;
-
-  int c = 0;
-  for (int w = w0; w < w1; ++w) c += __popcll(bm[w]);
-  cnt[tid] = c;
+  const int g = blockIdx.x;
+  for (int e = tid; e < N; e += 128) {
+    cnt[e] = a.counts[e];
+    tcnt[e] = (cnt[e] + kTileM - 1) / kTileM;
+  }
   __syncthreads();
-
-  if (tid < N) {
-    int s = 0;
-    for (int q = 0; q < P; ++q) s += cnt[tid * P + q];
-    ecount[tid] = s;
-    tcount[tid] = (s + kTileM - 1) / kTileM;
+  if (tid < 64) {
+    wave_scan_256(cnt, off, N, tid);
+    if (g == 0) wave_scan_256(tcnt, toff, N, tid);
   }
   __syncthreads();
 
-  if (tid < 64) {
-    // each lane scans 4 consecutive experts (N <= 256)
-    int loc[4], tloc[4];
-    int s = 0, ts = 0;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int ee = tid * 4 + j;
-      loc[j] = s;
-      tloc[j] = ts;
-      s += (ee < N) ? ecount[ee] : 0;
-      ts += (ee < N) ? tcount[ee] : 0;
-    }
-    const int incl = wave_inclusive_scan(s, tid);
-    const int tincl = wave_inclusive_scan(ts, tid);
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int ee = tid * 4 + j;
-      if (ee < N) {
-        eoff[ee] = incl - s + loc[j];
-        toff[ee] = tincl - ts + tloc[j];
+  if (g == 0) {
+    for (int e = tid; e <= N; e += 128) a.offsets[e] = off[e];
+    if (tid == 0) a.n_tiles[0] = toff[N];
+    for (int e = tid; e < N; e += 128) {
+      for (int j = 0; j < tcnt[e]; ++j) {
+        const int tg = toff[e] + j;
+        a.tile_expert[tg] = e;
+        a.tile_row0[tg] = off[e] + j * kTileM;
+        a.tile_rows[tg] = min(kTileM, cnt[e] - j * kTileM);
       }
     }
-    if (tid == 63) {
-      eoff[N] = incl;
-      toff[N] = tincl;
-    }
-  }
-  __syncthreads();
-
-  if (tid < N) {
-    a.counts[tid] = ecount[tid];
-    a.offsets[tid] = eoff[tid];
-    const int nt = tcount[tid];
-    for (int j = 0; j < nt; ++j) {
-      const int g = toff[tid] + j;
-      a.tile_expert[g] = tid;
-      a.tile_row0[g] = eoff[tid] + j * kTileM;
-      a.tile_rows[g] = min(kTileM, ecount[tid] - j * kTileM);
-    }
-  }
-  if (tid == 0) {
-    a.offsets[N] = eoff[N];
-    a.n_tiles[0] = toff[N];
   }
 
-  if (active) {
-    int row = eoff[e];
-    for (int q = 0; q < p; ++q) row += cnt[e * P + q];
-    for (int w = w0; w < w1; ++w) {
-      unsigned long long bits = bm[w];
-      while (bits) {
-        const int b = __builtin_ctzll(bits);
-        bits &= bits - 1ull;
-        const int t = w * 64 + b;
+  const int k = a.k;
+  if (tid < kRouteTokens * k) {
+    const int tl = tid / k;
+    const int t = g * kRouteTokens + tl;
+    if (t < a.T) {
+      const size_t o = static_cast<size_t>(t) * k + (tid - tl * k);
+      if (a.keep[o]) {
+        const int e = a.topk_idx[o];
+        const int row = off[e] + a.chunk_base[static_cast<size_t>(e) * a.G + g] + a.local_rank[o];
         a.perm[row] = t;
-        const int32_t *ids = a.topk_idx + static_cast<size_t>(t) * a.k;
-        for (int i = 0; i < a.k; ++i)
-          if (ids[i] == e) a.slot_row[static_cast<size_t>(t) * a.k + i] = row;
-        ++row;
+        a.slot_row[o] = row;
       }
     }
   }
@@ -128,7 +133,8 @@ __global__ __launch_bounds__(1024) void plan_kernel(PlanArgs a) {
 }  // namespace
 
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream) {
-  plan_kernel<<<dim3(1), 1024, 0, stream>>>(a);
+  expert_scan_kernel<<<dim3(a.N), 256, 0, stream>>>(a);
+  scatter_kernel<<<dim3(a.G), 128, 0, stream>>>(a);
   return hipGetLastError();
 }
 

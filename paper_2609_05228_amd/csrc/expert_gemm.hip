@@ -6,28 +6,44 @@
 // weights.
 //
 //   gateup: H[r, :] = SiLU(x_in[perm[r]] W_gate[e]^T) * (x_in[perm[r]] W_up[e]^T)
-//           (the A rows are gathered through perm while staging the tile;
-//           SiLU and the product are fused into the epilogue)
+//           (A rows gathered through perm; SiLU and the product fused into the
+//           epilogue)
 //   down:   Y[r, :] = H[r, :] W_down[e]^T
 //
-// bf16 path: bf16 MFMA (v_mfma_f32_16x16x32_bf16) with fp32 accumulation, tiles
-// staged through LDS with double buffering (one barrier per K step), padded LDS
-// rows (144 B) so the 16 rows an MFMA operand read touches hit distinct banks.
+// bf16 path (MI355X, bf16 MFMA v_mfma_f32_16x16x32_bf16, fp32 accumulation).
+// With 50% of 32768 slots kept over 128 experts an expert sees ~90-190 rows, so
+// the layer streams every activated expert's weights once and is HBM-bound:
+//  * an M tile holds up to 256 rows, so an expert's weights are read once per
+//    tile (a 128-row tile would re-read them for every expert past 128 rows);
+//    the row count selects one of five unrolled bodies (32..256 rows) so MFMAs
+//    and loads are issued only for the 16-row blocks a tile has;
+//  * operands move HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging)
+//    through two LDS rings: activations (L2-resident) 2-3 K stages deep, expert
+//    weights (from HBM) 5-8 stages deep, so ~80 KB of weights per CU are in
+//    flight; each wave waits only for the stage it computes next (vmcnt counted
+//    exactly from the issue schedule), then one barrier per K step;
+//  * one DMA instruction moves one MFMA fragment (16 rows x 32 k) and lane i
+//    lands at byte 16*i, which is exactly where lane i reads it back: LDS reads
+//    and writes are linear and bank-conflict free;
+//  * 4 waves as 2 x 2: a wave owns half the row blocks (interleaved, so short
+//    tiles stay balanced) and two column groups (gate/up: gate and up blocks of
+//    the same 16 features, so SwiGLU happens in registers; down: 32 columns).
 // fp32 path: plain tiled FMA (small parity workloads).
 //
 // Launch order is XCD-aware: workgroups are dealt to the 8 XCDs round-robin, so
 // block b runs on XCD b % 8; the N tiles of one M tile are mapped to one XCD so
-// the gathered activation rows they share stay in that XCD's L2.
+// the activation rows they share stay in that XCD's L2.
 #include "ace_internal.h"
 
 namespace ace {
 
 namespace {
 
-constexpr int BK = 64;        // K step
-constexpr int LDS_ROW = BK + 8;  // padded LDS row in elements (bf16: 144 B)
-constexpr int GU_BN = 64;     // gate/up: intermediate features per tile (x2 weight rows)
-constexpr int DN_BN = 128;    // down: output columns per tile
+constexpr int BK = 64;               // K per stage
+constexpr int kFragBytes = 1024;     // one MFMA fragment: 16 rows x 32 bf16
+constexpr int kLdsBytes = 144 * 1024;
+constexpr int GU_BN = 64;            // gate/up: intermediate features per tile
+constexpr int DN_BN = 128;           // down: output columns per tile
 
 struct TileInfo {
   int e, row0, rows;
@@ -57,218 +73,238 @@ __device__ __forceinline__ TileInfo tile_info(const GemmArgs &a, int grp) {
   return ti;
 }
 
-__device__ __forceinline__ f32x4_t mfma_bf16(bf16x8_t a, bf16x8_t b, f32x4_t c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }
 
-// stage 4 16-byte chunks of the A tile and 4 of the B tile.  A-tile rows past
-// the tile's row count read the last valid row instead: every output row depends
-// only on its own A row and those rows are never stored.
-__device__ __forceinline__ void gload4(uint4 (&ra)[4], uint4 (&rb)[4], const bf16_t *const (&asrc)[4],
-                                       const bf16_t *const (&bsrc)[4], int k0) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    ra[i] = *reinterpret_cast<const uint4 *>(asrc[i] + k0);
-    rb[i] = *reinterpret_cast<const uint4 *>(bsrc[i] + k0);
-  }
+__device__ __forceinline__ uint32_t lds_addr(const void *p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void *)p));
 }
 
-__device__ __forceinline__ void sstore4(bf16_t *as, bf16_t *bs, const uint4 (&ra)[4], const uint4 (&rb)[4],
-                                        const int (&loff)[4]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    *reinterpret_cast<uint4 *>(as + loff[i]) = ra[i];
-    *reinterpret_cast<uint4 *>(bs + loff[i]) = rb[i];
-  }
+// 16 bytes per lane from global `src` into LDS at lds_base + 16 * lane.  M0 is
+// saved and restored around the DMA so the compiler's use of it is unaffected.
+// The compiler does not see this LDS write: every consumer waits on vmcnt and
+// crosses a barrier explicitly.
+__device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+      : "memory");
 }
 
-// one BK step of the gate/up tile from LDS: wave (wm, wn) owns 64 rows x 32 features
-__device__ __forceinline__ void gateup_step(const bf16_t *As, const bf16_t *Bs, int wm, int wn, int r16, int kg,
-                                            f32x4_t (&accg)[4][2], f32x4_t (&accu)[4][2]) {
+__device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// wait until at most n (0..31) of this wave's vector memory operations are outstanding
+__device__ __forceinline__ void wait_vmcnt(int n) {
+#define ACE_VMCNT_CASE(c) \
+  case c:                 \
+    asm volatile("s_waitcnt vmcnt(" #c ")" ::: "memory"); \
+    break;
+  switch (n) {
+    ACE_VMCNT_CASE(0) ACE_VMCNT_CASE(1) ACE_VMCNT_CASE(2) ACE_VMCNT_CASE(3) ACE_VMCNT_CASE(4)
+    ACE_VMCNT_CASE(5) ACE_VMCNT_CASE(6) ACE_VMCNT_CASE(7) ACE_VMCNT_CASE(8) ACE_VMCNT_CASE(9)
+    ACE_VMCNT_CASE(10) ACE_VMCNT_CASE(11) ACE_VMCNT_CASE(12) ACE_VMCNT_CASE(13) ACE_VMCNT_CASE(14)
+    ACE_VMCNT_CASE(15) ACE_VMCNT_CASE(16) ACE_VMCNT_CASE(17) ACE_VMCNT_CASE(18) ACE_VMCNT_CASE(19)
+    ACE_VMCNT_CASE(20) ACE_VMCNT_CASE(21) ACE_VMCNT_CASE(22) ACE_VMCNT_CASE(23) ACE_VMCNT_CASE(24)
+    ACE_VMCNT_CASE(25) ACE_VMCNT_CASE(26) ACE_VMCNT_CASE(27) ACE_VMCNT_CASE(28) ACE_VMCNT_CASE(29)
+    ACE_VMCNT_CASE(30) ACE_VMCNT_CASE(31)
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
+#undef ACE_VMCNT_CASE
+}
+
+// Pipeline geometry for a tile of MB 16-row blocks.  A (activation rows, mostly
+// L2 hits) and B (expert weights, streamed from HBM) have their own LDS rings:
+// A is prefetched SA-1 stages ahead, B SB-1 stages ahead, SB as deep as LDS
+// allows after the A ring.
+template <int MB> struct Pipe {
+  static constexpr int NA = MB / 2;                 // A DMAs per wave per stage
+  static constexpr int NB = 4;                      // B DMAs per wave per stage
+  static constexpr int ASZ = 2 * MB * kFragBytes;   // A stage: MB row blocks x 2 k halves
+  static constexpr int BSZ = 16 * kFragBytes;       // B stage: 8 column blocks x 2 k halves
+  static constexpr int SA = MB >= 12 ? 2 : 3;
+  static constexpr int SB0 = (kLdsBytes - SA * ASZ) / BSZ;
+  static constexpr int SB = SB0 > 8 ? 8 : SB0;
+  static_assert(SB >= 3, "B ring too shallow");
+  static_assert(NB + NA + NB <= 31, "outstanding DMAs exceed the wait table");
+};
+
+// DMAs this wave issued after the A part of stage kt, at the wait before stage
+// kt's compute.  Issue order: prologue B(0..SB-2), A(0..SA-2); then iteration j
+// (after its barrier) issues A(j+SA-1) and B(j+SB-1) when they exist.  vmcnt
+// completes in order, so once A(kt) is done, B(kt) (issued earlier) is too.
+template <int MB>
+__device__ __forceinline__ int ops_after_a(int kt, int nk) {
+  using P = Pipe<MB>;
+  int n = 0;
+  if (kt <= P::SA - 2)
+    n += max(0, min(P::SA - 1, nk) - 1 - kt) * P::NA;  // later prologue A stages that exist
+  else if (kt - P::SA + 1 + P::SB - 1 < nk)
+    n += P::NB;
+  for (int j = max(0, kt - P::SA + 2); j < kt; ++j)
+    n += (j + P::SA - 1 < nk ? P::NA : 0) + (j + P::SB - 1 < nk ? P::NB : 0);
+  return n;
+}
+
+// One M tile x one N tile with MB 16-row blocks (MB even, <= 16).
+// Waves form a 2 x 2 grid: wave (wr, wc) computes the interleaved row blocks
+// wr, wr+2, ... against column groups 2wc and 2wc+1 (gate/up: 16 features each,
+// as a gate block and an up block; down: 32 output columns each).
+template <bool GATEUP, int MB>
+__device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, uint8_t *smem) {
+  using P = Pipe<MB>;
+  constexpr int NA = P::NA, SA = P::SA, SB = P::SB;
+  constexpr int MW = MB / 2;  // row blocks per wave
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int wr = wave >> 1, wc = wave & 1;
+  const int K = GATEUP ? a.d : a.m;
+  const bf16_t *act = static_cast<const bf16_t *>(a.act);
+
+  // A fragments this wave stages: f = wave + 4 j -> row block f / 2, k half f % 2
+  const bf16_t *asrc[NA];
 #pragma unroll
-  for (int kk = 0; kk < BK; kk += 32) {
-    bf16x8_t af[4], bg[2], bu[2];
+  for (int j = 0; j < NA; ++j) {
+    const int f = wave + 4 * j;
+    const int row = min((f >> 1) * 16 + r16, ti.rows - 1);  // rows past the tile repeat its last row
+    const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
+    asrc[j] = act + static_cast<size_t>(src_row) * K + (f & 1) * 32 + 8 * g;
+  }
+  // B fragments this wave stages: column group `wave` (two 16-column blocks x two k halves)
+  const bf16_t *bsrc[2];
+  if (GATEUP) {
+    const size_t f = static_cast<size_t>(ti.e) * a.m + nt * GU_BN + wave * 16 + r16;
+    bsrc[0] = static_cast<const bf16_t *>(a.w0) + f * a.d + 8 * g;
+    bsrc[1] = static_cast<const bf16_t *>(a.w1) + f * a.d + 8 * g;
+  } else {
+    const size_t n = static_cast<size_t>(ti.e) * a.d + nt * DN_BN + wave * 32 + r16;
+    bsrc[0] = static_cast<const bf16_t *>(a.w0) + n * a.m + 8 * g;
+    bsrc[1] = bsrc[0] + static_cast<size_t>(16) * a.m;
+  }
+  const uint32_t ldsA = lds_addr(smem);
+  const uint32_t ldsB = ldsA + SA * P::ASZ;
+  const uint8_t *smemA = smem;
+  const uint8_t *smemB = smem + SA * P::ASZ;
+
+  f32x4_t acc[MW][4];
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-      af[mi] = *reinterpret_cast<const bf16x8_t *>(&As[(wm * 64 + mi * 16 + r16) * LDS_ROW + kk + kg]);
+  for (int i = 0; i < MW; ++i)
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      bg[ni] = *reinterpret_cast<const bf16x8_t *>(&Bs[(wn * 32 + ni * 16 + r16) * LDS_ROW + kk + kg]);
-      bu[ni] = *reinterpret_cast<const bf16x8_t *>(&Bs[(GU_BN + wn * 32 + ni * 16 + r16) * LDS_ROW + kk + kg]);
+    for (int c = 0; c < 4; ++c) acc[i][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  const int nk = K / BK;
+  // prologue: B stages 0..SB-2, then A stages 0..SA-2
+  for (int s = 0; s < SB - 1 && s < nk; ++s) {
+    const uint32_t st = ldsB + s * P::BSZ;
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) dma16(bsrc[cb] + s * BK + 32 * h, st + (wave * 4 + cb * 2 + h) * kFragBytes);
+  }
+  for (int s = 0; s < SA - 1 && s < nk; ++s) {
+    const uint32_t st = ldsA + s * P::ASZ;
+#pragma unroll
+    for (int j = 0; j < NA; ++j) dma16(asrc[j] + s * BK, st + (wave + 4 * j) * kFragBytes);
+  }
+
+  for (int kt = 0; kt < nk; ++kt) {
+    wait_vmcnt(ops_after_a<MB>(kt, nk));
+    barrier();  // stage kt landed for every wave; every wave is done with stage kt-1
+    if (kt + SA - 1 < nk) {
+      const int s = kt + SA - 1;
+      const uint32_t st = ldsA + (s % SA) * P::ASZ;
+#pragma unroll
+      for (int j = 0; j < NA; ++j) dma16(asrc[j] + s * BK, st + (wave + 4 * j) * kFragBytes);
     }
+    if (kt + SB - 1 < nk) {
+      const int s = kt + SB - 1;
+      const uint32_t st = ldsB + (s % SB) * P::BSZ;
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+      for (int cb = 0; cb < 2; ++cb)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni) {
-        accg[mi][ni] = mfma_bf16(af[mi], bg[ni], accg[mi][ni]);
-        accu[mi][ni] = mfma_bf16(af[mi], bu[ni], accu[mi][ni]);
+        for (int h = 0; h < 2; ++h) dma16(bsrc[cb] + s * BK + 32 * h, st + (wave * 4 + cb * 2 + h) * kFragBytes);
+    }
+    const uint8_t *sa = smemA + (kt % SA) * P::ASZ;
+    const uint8_t *sb = smemB + (kt % SB) * P::BSZ;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      bf16x8_t b[4];  // [fl * 2 + cb]: column group 2wc + fl, block cb
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        b[c] = *reinterpret_cast<const bf16x8_t *>(sb + ((2 * wc + (c >> 1)) * 4 + (c & 1) * 2 + h) * kFragBytes +
+                                                   16 * lane);
+#pragma unroll
+      for (int i = 0; i < MW; ++i) {
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t *>(sa + (2 * (2 * i + wr) + h) * kFragBytes + 16 * lane);
+#pragma unroll
+        for (int c = 0; c < 4; ++c) acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, b[c], acc[i][c], 0, 0, 0);
       }
-  }
-}
-
-// one BK step of the down tile from LDS: wave (wm, wn) owns 64 rows x 64 columns
-__device__ __forceinline__ void down_step(const bf16_t *As, const bf16_t *Bs, int wm, int wn, int r16, int kg,
-                                          f32x4_t (&acc)[4][4]) {
-#pragma unroll
-  for (int kk = 0; kk < BK; kk += 32) {
-    bf16x8_t af[4], bf[4];
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-      af[mi] = *reinterpret_cast<const bf16x8_t *>(&As[(wm * 64 + mi * 16 + r16) * LDS_ROW + kk + kg]);
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni)
-      bf[ni] = *reinterpret_cast<const bf16x8_t *>(&Bs[(wn * 64 + ni * 16 + r16) * LDS_ROW + kk + kg]);
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = mfma_bf16(af[mi], bf[ni], acc[mi][ni]);
-  }
-}
-
-// ------------------------------------------------------------------ bf16 gate/up
-__global__ __launch_bounds__(256) void gateup_bf16_kernel(GemmArgs a) {
-  const int nN = a.m / GU_BN;
-  int grp, nt;
-  map_block(blockIdx.x, nN, &grp, &nt);
-  const TileInfo ti = tile_info(a, grp);
-  if (!ti.valid) return;
-
-  __shared__ __align__(16) bf16_t As[2][kTileM * LDS_ROW];
-  __shared__ __align__(16) bf16_t Bs[2][2 * GU_BN * LDS_ROW];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int d = a.d, m = a.m;
-  const int f0 = nt * GU_BN;
-  const bf16_t *xn = static_cast<const bf16_t *>(a.act);
-  const bf16_t *wg = static_cast<const bf16_t *>(a.w0);
-  const bf16_t *wu = static_cast<const bf16_t *>(a.w1);
-
-  // each thread stages 4 16-byte chunks of the A tile and 4 of the B tile per K step
-  const bf16_t *asrc[4];
-  const bf16_t *bsrc[4];
-  int loff[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i;
-    const int r = c >> 3, c8 = c & 7;
-    loff[i] = r * LDS_ROW + c8 * 8;
-    const int rr = min(r, ti.rows - 1);
-    const int tok = a.perm ? a.perm[ti.row0 + rr] : ti.row0 + rr;
-    asrc[i] = xn + static_cast<size_t>(tok) * d + c8 * 8;
-    const bf16_t *w = (r < GU_BN) ? wg : wu;
-    bsrc[i] = w + (static_cast<size_t>(ti.e) * m + f0 + (r & (GU_BN - 1))) * d + c8 * 8;
-  }
-  uint4 ra[4], rb[4];
-  const int wm = wave >> 1, wn = wave & 1;
-  const int r16 = lane & 15, kg = (lane >> 4) * 8;
-  f32x4_t accg[4][2], accu[4][2];
-#pragma unroll
-  for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < 2; ++ni) {
-      accg[mi][ni] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      accu[mi][ni] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
-
-  const int nk = d / BK;
-  gload4(ra, rb, asrc, bsrc, 0);
-  sstore4(As[0], Bs[0], ra, rb, loff);
-  __syncthreads();
-  for (int kt = 0; kt < nk - 1; ++kt) {
-    const int buf = kt & 1;
-    gload4(ra, rb, asrc, bsrc, (kt + 1) * BK);
-    gateup_step(As[buf], Bs[buf], wm, wn, r16, kg, accg, accu);
-    sstore4(As[buf ^ 1], Bs[buf ^ 1], ra, rb, loff);
-    __syncthreads();
   }
-  gateup_step(As[(nk - 1) & 1], Bs[(nk - 1) & 1], wm, wn, r16, kg, accg, accu);
 
-  bf16_t *H = static_cast<bf16_t *>(a.out);
+  // epilogue: lane holds column r16 of each block, rows 4*g + q
 #pragma unroll
-  for (int mi = 0; mi < 4; ++mi)
+  for (int fl = 0; fl < 2; ++fl) {
+    const int grp = 2 * wc + fl;
+    if (GATEUP) {
+      bf16_t *H = static_cast<bf16_t *>(a.out);
+      const int f = nt * GU_BN + grp * 16 + r16;
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+      for (int i = 0; i < MW; ++i)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = wm * 64 + mi * 16 + (lane >> 4) * 4 + i;
-        const int f = f0 + wn * 32 + ni * 16 + r16;
-        if (r < ti.rows) {
-          const float h = silu(accg[mi][ni][i]) * accu[mi][ni][i];
-          H[static_cast<size_t>(ti.row0 + r) * m + f] = f32_to_bf16(h);
+        for (int q = 0; q < 4; ++q) {
+          const int row = (2 * i + wr) * 16 + 4 * g + q;
+          if (row < ti.rows)
+            H[static_cast<size_t>(ti.row0 + row) * a.m + f] =
+                f32_to_bf16(silu(acc[i][fl * 2][q]) * acc[i][fl * 2 + 1][q]);
         }
-      }
+    } else {
+      bf16_t *Y = static_cast<bf16_t *>(a.out);
+      const int n = nt * DN_BN + grp * 32 + r16;
+#pragma unroll
+      for (int i = 0; i < MW; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = (2 * i + wr) * 16 + 4 * g + q;
+          if (row < ti.rows) {
+            bf16_t *yr = Y + static_cast<size_t>(ti.row0 + row) * a.d + n;
+            yr[0] = f32_to_bf16(acc[i][fl * 2][q]);
+            yr[16] = f32_to_bf16(acc[i][fl * 2 + 1][q]);
+          }
+        }
+    }
+  }
 }
 
-// ------------------------------------------------------------------ bf16 down
-__global__ __launch_bounds__(256) void down_bf16_kernel(GemmArgs a) {
-  const int nN = a.d / DN_BN;
+template <bool GATEUP>
+__global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
+  const int nN = GATEUP ? a.m / GU_BN : a.d / DN_BN;
   int grp, nt;
   map_block(blockIdx.x, nN, &grp, &nt);
   const TileInfo ti = tile_info(a, grp);
   if (!ti.valid) return;
-
-  __shared__ __align__(16) bf16_t As[2][kTileM * LDS_ROW];
-  __shared__ __align__(16) bf16_t Bs[2][DN_BN * LDS_ROW];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int d = a.d, m = a.m;
-  const int n0 = nt * DN_BN;
-  const bf16_t *H = static_cast<const bf16_t *>(a.act);
-  const bf16_t *wd = static_cast<const bf16_t *>(a.w0);
-
-  const bf16_t *asrc[4];
-  const bf16_t *bsrc[4];
-  int loff[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int c = tid + 256 * i;
-    const int r = c >> 3, c8 = c & 7;
-    loff[i] = r * LDS_ROW + c8 * 8;
-    asrc[i] = H + static_cast<size_t>(ti.row0 + min(r, ti.rows - 1)) * m + c8 * 8;
-    bsrc[i] = wd + (static_cast<size_t>(ti.e) * d + n0 + r) * m + c8 * 8;
-  }
-
-  uint4 ra[4], rb[4];
-
-  const int wm = wave >> 1, wn = wave & 1;
-  const int r16 = lane & 15, kg = (lane >> 4) * 8;
-  f32x4_t acc[4][4];
-#pragma unroll
-  for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  const int nk = m / BK;
-  gload4(ra, rb, asrc, bsrc, 0);
-  sstore4(As[0], Bs[0], ra, rb, loff);
-  __syncthreads();
-  for (int kt = 0; kt < nk - 1; ++kt) {
-    const int buf = kt & 1;
-    gload4(ra, rb, asrc, bsrc, (kt + 1) * BK);
-    down_step(As[buf], Bs[buf], wm, wn, r16, kg, acc);
-    sstore4(As[buf ^ 1], Bs[buf ^ 1], ra, rb, loff);
-    __syncthreads();
-  }
-  down_step(As[(nk - 1) & 1], Bs[(nk - 1) & 1], wm, wn, r16, kg, acc);
-
-  bf16_t *Y = static_cast<bf16_t *>(a.out);
-#pragma unroll
-  for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-    for (int ni = 0; ni < 4; ++ni)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int r = wm * 64 + mi * 16 + (lane >> 4) * 4 + i;
-        const int n = n0 + wn * 64 + ni * 16 + r16;
-        if (r < ti.rows) Y[static_cast<size_t>(ti.row0 + r) * d + n] = f32_to_bf16(acc[mi][ni][i]);
-      }
+  __shared__ __align__(16) uint8_t smem[kLdsBytes];
+  const int blocks = (ti.rows + 15) >> 4;
+  if (blocks <= 2)
+    gemm_tile<GATEUP, 2>(a, ti, nt, smem);
+  else if (blocks <= 4)
+    gemm_tile<GATEUP, 4>(a, ti, nt, smem);
+  else if (blocks <= 8)
+    gemm_tile<GATEUP, 8>(a, ti, nt, smem);
+  else if (blocks <= 12)
+    gemm_tile<GATEUP, 12>(a, ti, nt, smem);
+  else
+    gemm_tile<GATEUP, 16>(a, ti, nt, smem);
 }
 
 // ------------------------------------------------------------------ fp32 (tiled FMA)
 constexpr int F_BN = 16;
 constexpr int F_BK = 16;
+constexpr int F_RPT = kTileM / 16;  // rows per thread
 
 __global__ __launch_bounds__(256) void gateup_f32_kernel(GemmArgs a) {
   const int nN = a.m / F_BN;
@@ -284,19 +320,18 @@ __global__ __launch_bounds__(256) void gateup_f32_kernel(GemmArgs a) {
   const float *xn = static_cast<const float *>(a.act);
   const float *wg = static_cast<const float *>(a.w0);
   const float *wu = static_cast<const float *>(a.w1);
-  int tok[8];
+  float ag[F_RPT], au[F_RPT];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int r = (tid + 256 * j) >> 4;
-    tok[j] = (r < ti.rows) ? (a.perm ? a.perm[ti.row0 + r] : ti.row0 + r) : -1;
-  }
-  float ag[8] = {0}, au[8] = {0};
+  for (int i = 0; i < F_RPT; ++i) ag[i] = au[i] = 0.f;
   for (int k0 = 0; k0 < d; k0 += F_BK) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = tid + 256 * j;
+    for (int c = tid; c < kTileM * F_BK; c += 256) {
       const int r = c >> 4, kk = c & 15;
-      As[r][kk] = (tok[j] >= 0) ? xn[static_cast<size_t>(tok[j]) * d + k0 + kk] : 0.f;
+      float v = 0.f;
+      if (r < ti.rows) {
+        const int tok = a.perm ? a.perm[ti.row0 + r] : ti.row0 + r;
+        v = xn[static_cast<size_t>(tok) * d + k0 + kk];
+      }
+      As[r][kk] = v;
     }
     {
       const int r = tid >> 4, kk = tid & 15;
@@ -309,7 +344,7 @@ __global__ __launch_bounds__(256) void gateup_f32_kernel(GemmArgs a) {
     for (int kk = 0; kk < F_BK; ++kk) {
       const float bgv = Bg[tx][kk], buv = Bu[tx][kk];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
+      for (int i = 0; i < F_RPT; ++i) {
         ag[i] = fmaf(As[ty + 16 * i][kk], bgv, ag[i]);
         au[i] = fmaf(As[ty + 16 * i][kk], buv, au[i]);
       }
@@ -318,7 +353,7 @@ __global__ __launch_bounds__(256) void gateup_f32_kernel(GemmArgs a) {
   }
   float *H = static_cast<float *>(a.out);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < F_RPT; ++i) {
     const int r = ty + 16 * i;
     if (r < ti.rows) H[static_cast<size_t>(ti.row0 + r) * m + f0 + tx] = silu(ag[i]) * au[i];
   }
@@ -336,11 +371,11 @@ __global__ __launch_bounds__(256) void down_f32_kernel(GemmArgs a) {
   const int d = a.d, m = a.m, n0 = nt * F_BN;
   const float *H = static_cast<const float *>(a.act);
   const float *wd = static_cast<const float *>(a.w0);
-  float acc[8] = {0};
-  for (int k0 = 0; k0 < m; k0 += F_BK) {
+  float acc[F_RPT];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int c = tid + 256 * j;
+  for (int i = 0; i < F_RPT; ++i) acc[i] = 0.f;
+  for (int k0 = 0; k0 < m; k0 += F_BK) {
+    for (int c = tid; c < kTileM * F_BK; c += 256) {
       const int r = c >> 4, kk = c & 15;
       As[r][kk] = (r < ti.rows) ? H[static_cast<size_t>(ti.row0 + r) * m + k0 + kk] : 0.f;
     }
@@ -353,13 +388,13 @@ __global__ __launch_bounds__(256) void down_f32_kernel(GemmArgs a) {
     for (int kk = 0; kk < F_BK; ++kk) {
       const float bv = Bs[tx][kk];
 #pragma unroll
-      for (int i = 0; i < 8; ++i) acc[i] = fmaf(As[ty + 16 * i][kk], bv, acc[i]);
+      for (int i = 0; i < F_RPT; ++i) acc[i] = fmaf(As[ty + 16 * i][kk], bv, acc[i]);
     }
     __syncthreads();
   }
   float *Y = static_cast<float *>(a.out);
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
+  for (int i = 0; i < F_RPT; ++i) {
     const int r = ty + 16 * i;
     if (r < ti.rows) Y[static_cast<size_t>(ti.row0 + r) * d + n0 + tx] = acc[i];
   }
@@ -375,7 +410,7 @@ unsigned grid_for(int max_groups, int nN) {
 hipError_t launch_gateup(const GemmArgs &a, bool bf16, hipStream_t stream) {
   if (a.max_groups <= 0) return hipSuccess;
   if (bf16)
-    gateup_bf16_kernel<<<dim3(grid_for(a.max_groups, a.m / GU_BN)), 256, 0, stream>>>(a);
+    grouped_gemm_bf16_kernel<true><<<dim3(grid_for(a.max_groups, a.m / GU_BN)), 256, 0, stream>>>(a);
   else
     gateup_f32_kernel<<<dim3(grid_for(a.max_groups, a.m / F_BN)), 256, 0, stream>>>(a);
   return hipGetLastError();
@@ -384,7 +419,7 @@ hipError_t launch_gateup(const GemmArgs &a, bool bf16, hipStream_t stream) {
 hipError_t launch_down(const GemmArgs &a, bool bf16, hipStream_t stream) {
   if (a.max_groups <= 0) return hipSuccess;
   if (bf16)
-    down_bf16_kernel<<<dim3(grid_for(a.max_groups, a.d / DN_BN)), 256, 0, stream>>>(a);
+    grouped_gemm_bf16_kernel<false><<<dim3(grid_for(a.max_groups, a.d / DN_BN)), 256, 0, stream>>>(a);
   else
     down_f32_kernel<<<dim3(grid_for(a.max_groups, a.d / F_BN)), 256, 0, stream>>>(a);
   return hipGetLastError();

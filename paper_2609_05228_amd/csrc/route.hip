@@ -8,53 +8,129 @@
 //     (v_mfma_f32_16x16x4f32): x_in is the un-rounded fp32 RMSNorm output, so the
 //     top-k and skip decisions see fp32 logits, not bf16-rounded activations.
 //     Wave w owns a quarter of the hidden dimension and keeps two accumulator
-//     sets (alternating 16-wide K blocks); the 8 partial sums per logit are added
+//     sets (alternating 32-wide K blocks); the 8 partial sums per logit are added
 //     in a fixed order, which keeps the accumulated rounding near 2e-7 for
 //     d = 2048.  The same pass writes x_in, rounded to the GEMM dtype, for the
 //     expert GEMMs.
-//  3. Each wave takes 4 tokens: top-k by k rounds of a wavefront arg-max (ties go
-//     to the lower expert id), gates g = exp(z_i - z_1) / sum_j exp(z_j - z_1)
-//     over the k selected logits (the softmax over all N experts cancels in the
-//     renormalised gate), then Alg. 4 evaluated redundantly in every lane (k <= 8
-//     scalars), and lane i < k writes slot i.  Kept (expert, token) pairs are
-//     recorded in a per-expert token bitmap with integer atomic OR, which makes
-//     the later dispatch order independent of scheduling.
+//     The hidden dimension is walked in 32-wide blocks (16-byte loads per lane)
+//     with the next block's operands loaded before the current block's MFMAs.
+//  3. Each 16-lane group of a wave takes one token (4 tokens per wave at once):
+//     top-k by k rounds of a 16-lane arg-max (ties go to the lower expert id),
+//     gates g = exp(z_i - z_1) / sum_j exp(z_j - z_1) over the k selected logits
+//     (the softmax over all N experts cancels in the renormalised gate), then
+//     Alg. 4 evaluated redundantly in every lane of the group (k <= 8 scalars),
+//     and lane i < k of the group writes slot i.
+//  4. For the dispatch plan, each kept slot gets its rank among this
+//     workgroup's kept slots of the same expert in token order (from a 16-bit
+//     token mask per expert in LDS), and the workgroup writes its per-expert
+//     kept counts.  No global atomics: the plan is independent of scheduling.
 #include "ace_internal.h"
 
 namespace ace {
 
 namespace {
 
-constexpr int kTok = 16;  // tokens per workgroup
+constexpr int kTok = kRouteTokens;  // tokens per workgroup
 
-template <typename T> struct Vec4;
-template <> struct Vec4<float> {
-  static __device__ __forceinline__ void load(const float *p, float v[4]) {
-    const float4 q = *reinterpret_cast<const float4 *>(p);
-    v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+// 8 consecutive elements: raw storage and conversion
+template <typename T> struct Oct;
+template <> struct Oct<float> {
+  struct raw {
+    float4 lo, hi;
+  };
+  static __device__ __forceinline__ raw load(const float *p) {
+    raw r;
+    r.lo = *reinterpret_cast<const float4 *>(p);
+    r.hi = *reinterpret_cast<const float4 *>(p + 4);
+    return r;
   }
-  static __device__ __forceinline__ void store(float *p, const float v[4]) {
+  static __device__ __forceinline__ void cvt(const raw &q, float v[8]) {
+    v[0] = q.lo.x; v[1] = q.lo.y; v[2] = q.lo.z; v[3] = q.lo.w;
+    v[4] = q.hi.x; v[5] = q.hi.y; v[6] = q.hi.z; v[7] = q.hi.w;
+  }
+  static __device__ __forceinline__ void store(float *p, const float v[8]) {
     *reinterpret_cast<float4 *>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    *reinterpret_cast<float4 *>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
   }
 };
-template <> struct Vec4<bf16_t> {
-  static __device__ __forceinline__ void load(const bf16_t *p, float v[4]) {
-    const uint2 q = *reinterpret_cast<const uint2 *>(p);
-    v[0] = __uint_as_float(q.x << 16);
-    v[1] = __uint_as_float(q.x & 0xFFFF0000u);
-    v[2] = __uint_as_float(q.y << 16);
-    v[3] = __uint_as_float(q.y & 0xFFFF0000u);
+template <> struct Oct<bf16_t> {
+  typedef uint4 raw;
+  static __device__ __forceinline__ raw load(const bf16_t *p) { return *reinterpret_cast<const uint4 *>(p); }
+  static __device__ __forceinline__ void cvt(const raw &q, float v[8]) {
+    const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[2 * j] = __uint_as_float(w[j] << 16);
+      v[2 * j + 1] = __uint_as_float(w[j] & 0xFFFF0000u);
+    }
   }
-  static __device__ __forceinline__ void store(bf16_t *p, const float v[4]) {
-    uint2 q;
-    q.x = static_cast<uint32_t>(f32_to_bf16(v[0])) | (static_cast<uint32_t>(f32_to_bf16(v[1])) << 16);
-    q.y = static_cast<uint32_t>(f32_to_bf16(v[2])) | (static_cast<uint32_t>(f32_to_bf16(v[3])) << 16);
-    *reinterpret_cast<uint2 *>(p) = q;
+  static __device__ __forceinline__ void store(bf16_t *p, const float v[8]) {
+    uint32_t w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      w[j] = static_cast<uint32_t>(f32_to_bf16(v[2 * j])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * j + 1])) << 16);
+    *reinterpret_cast<uint4 *>(p) = make_uint4(w[0], w[1], w[2], w[3]);
   }
 };
+
+template <typename T>
+__device__ __forceinline__ void load4(const T *p, float v[4]);
+template <>
+__device__ __forceinline__ void load4<float>(const float *p, float v[4]) {
+  const float4 q = *reinterpret_cast<const float4 *>(p);
+  v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+}
+template <>
+__device__ __forceinline__ void load4<bf16_t>(const bf16_t *p, float v[4]) {
+  const uint2 q = *reinterpret_cast<const uint2 *>(p);
+  v[0] = __uint_as_float(q.x << 16);
+  v[1] = __uint_as_float(q.x & 0xFFFF0000u);
+  v[2] = __uint_as_float(q.y << 16);
+  v[3] = __uint_as_float(q.y & 0xFFFF0000u);
+}
 
 __device__ __forceinline__ bool better(float v, int e, float bv, int be) {
   return v > bv || (v == bv && e < be);
+}
+
+// Operands of one 32-wide K block for one lane: the lane's 8 consecutive k of
+// its token row, of gamma and of NT router rows.  MFMA j of the block takes
+// element j from every lane, so lane group g supplies k = kb + 8g + j to both
+// operands and the block covers kb .. kb + 31.
+template <typename T, int NT> struct Block {
+  typename Oct<T>::raw x, g, w[NT];
+};
+
+template <typename T, int NT>
+__device__ __forceinline__ void load_block(Block<T, NT> &b, const T *xrow, const T *gamma, const T *wr,
+                                           int d, int N, int r16, int k) {
+  b.x = Oct<T>::load(xrow + k);
+  b.g = Oct<T>::load(gamma + k);
+#pragma unroll
+  for (int et = 0; et < NT; ++et) {
+    const int e = min(et * 16 + r16, N - 1);  // rows past N reuse row N-1; their logits are never read
+    b.w[et] = Oct<T>::load(wr + static_cast<size_t>(e) * d + k);
+  }
+}
+
+template <typename T, int NT>
+__device__ __forceinline__ void mfma_block(const Block<T, NT> &b, f32x4_t (&acc)[NT], float rs, bool tvalid,
+                                           T *xnp) {
+  float xv[8], gv[8], av[8];
+  Oct<T>::cvt(b.x, xv);
+  Oct<T>::cvt(b.g, gv);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) av[j] = tvalid ? (xv[j] * rs) * gv[j] : 0.f;
+  if (tvalid) Oct<T>::store(xnp, av);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+#pragma unroll
+    for (int et = 0; et < NT; ++et) {
+      float bv[8];
+      Oct<T>::cvt(b.w[et], bv);
+      acc[et] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], bv[j], acc[et], 0, 0, 0);
+    }
+  }
 }
 
 // NT = number of 16-expert tiles covered (N <= 16 * NT)
@@ -67,6 +143,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
 
   __shared__ float rstd_s[kTok];
   __shared__ float zp[4][kTok][NT * 16 + 1];
+  __shared__ uint32_t emask[NT * 16];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -74,6 +151,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
   const int t0 = blockIdx.x * kTok;
   const int d = a.d;
   const int N = a.N;
+  for (int e = tid; e < NT * 16; e += 256) emask[e] = 0u;
 
   // ---- 1. RMS scale per token
   for (int j = 0; j < 4; ++j) {
@@ -84,7 +162,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
       const T *row = x + static_cast<size_t>(t) * d;
       for (int c = lane * 4; c < d; c += 256) {
         float v[4];
-        Vec4<T>::load(row + c, v);
+        load4<T>(row + c, v);
         ss = fmaf(v[0], v[0], ss);
         ss = fmaf(v[1], v[1], ss);
         ss = fmaf(v[2], v[2], ss);
@@ -96,53 +174,42 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
   }
   __syncthreads();
 
-  // ---- 2. router logits on fp32 MFMA
+  // ---- 2. router logits on fp32 MFMA, two accumulator sets (even / odd K blocks)
   {
     const int r16 = lane & 15;  // A row (token) / B column (expert within a tile)
     const int grp = lane >> 4;  // K group of the MFMA operand
     const int t = t0 + r16;
     const bool tvalid = t < a.T;
     const float rs = rstd_s[r16];
-    const int kq = d >> 2;
-    const int kbeg = wave * kq;
+    const int kq = d >> 2;         // this wave's K range, a multiple of 32
+    const int nb = kq >> 5;        // 32-wide K blocks
+    const int kbeg = wave * kq + grp * 8;
     const T *xrow = x + static_cast<size_t>(tvalid ? t : 0) * d;
     T *xnrow = xn + static_cast<size_t>(tvalid ? t : 0) * d;
 
-    f32x4_t acc[2][NT];
+    f32x4_t acc0[NT], acc1[NT];
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
-#pragma unroll
-      for (int et = 0; et < NT; ++et) acc[s][et] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-    for (int kb = kbeg; kb < kbeg + kq; kb += 32) {
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const int k = kb + s * 16 + grp * 4;
-        float av[4] = {0.f, 0.f, 0.f, 0.f};
-        if (tvalid) {
-          float xv[4], gv[4];
-          Vec4<T>::load(xrow + k, xv);
-          Vec4<T>::load(gamma + k, gv);
-#pragma unroll
-          for (int j = 0; j < 4; ++j) av[j] = (xv[j] * rs) * gv[j];
-          Vec4<T>::store(xnrow + k, av);
-        }
-#pragma unroll
-        for (int et = 0; et < NT; ++et) {
-          const int e = et * 16 + r16;
-          float bv[4] = {0.f, 0.f, 0.f, 0.f};
-          if (e < N) Vec4<T>::load(wr + static_cast<size_t>(e) * d + k, bv);
-#pragma unroll
-          for (int j = 0; j < 4; ++j)
-            acc[s][et] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], bv[j], acc[s][et], 0, 0, 0);
-        }
-      }
+    for (int et = 0; et < NT; ++et) {
+      acc0[et] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      acc1[et] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
+    // the next block's operands are loaded before the current block's MFMAs
+    Block<T, NT> b0, b1;
+    load_block<T, NT>(b0, xrow, gamma, wr, d, N, r16, kbeg);
+    int j = 0;
+    for (; j + 1 < nb; j += 2) {
+      const int k = kbeg + 32 * j;
+      load_block<T, NT>(b1, xrow, gamma, wr, d, N, r16, k + 32);
+      mfma_block<T, NT>(b0, acc0, rs, tvalid, xnrow + k);
+      load_block<T, NT>(b0, xrow, gamma, wr, d, N, r16, kbeg + 32 * min(j + 2, nb - 1));
+      mfma_block<T, NT>(b1, acc1, rs, tvalid, xnrow + k + 32);
+    }
+    if (j < nb) mfma_block<T, NT>(b0, acc0, rs, tvalid, xnrow + kbeg + 32 * j);
     // D[row = token 4*grp + i][col = expert et*16 + r16]
 #pragma unroll
     for (int et = 0; et < NT; ++et)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) zp[wave][grp * 4 + i][et * 16 + r16] = acc[0][et][i] + acc[1][et][i];
+      for (int i = 0; i < 4; ++i) zp[wave][grp * 4 + i][et * 16 + r16] = acc0[et][i] + acc1[et][i];
   }
   __syncthreads();
   for (int idx = tid; idx < kTok * N; idx += 256) {
@@ -154,17 +221,20 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
   }
   __syncthreads();
 
-  // ---- 3. top-k, gates and Alg. 4, one token at a time per wave
+  // ---- 3. top-k, gates and Alg. 4: one token per 16-lane group
   const int k = a.k;
-  for (int j = 0; j < 4; ++j) {
-    const int tl = wave * 4 + j;
-    const int t = t0 + tl;
-    if (t >= a.T) break;
+  const int sub = lane & 15;
+  const int tl = wave * 4 + (lane >> 4);
+  const int t = t0 + tl;
+  const bool tvalid = t < a.T;
+  int my_e = -1;        // expert of this lane's slot (lane sub < k), -1 if none
+  bool my_kept = false;
+  {
     const float *zrow = zp[0][tl];
-    float v[4];
+    float v[NT];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = lane + 64 * q;
+    for (int q = 0; q < NT; ++q) {
+      const int e = sub + 16 * q;
       v[q] = (e < N) ? zrow[e] : -INFINITY;
     }
     unsigned taken = 0;
@@ -178,16 +248,17 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
         float bv = -INFINITY;
         int be = 0x7fffffff;
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int e = lane + 64 * q;
+        for (int q = 0; q < NT; ++q) {
+          const int e = sub + 16 * q;
           if (e < N && !((taken >> q) & 1u) && better(v[q], e, bv, be)) {
             bv = v[q];
             be = e;
           }
         }
-        for (int off = 32; off > 0; off >>= 1) {
-          const float ov = __shfl_xor(bv, off);
-          const int oe = __shfl_xor(be, off);
+#pragma unroll
+        for (int off = 8; off > 0; off >>= 1) {
+          const float ov = __shfl_xor(bv, off, 16);
+          const int oe = __shfl_xor(be, off, 16);
           if (better(ov, oe, bv, be)) {
             bv = ov;
             be = oe;
@@ -195,7 +266,7 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
         }
         sel_e[i] = be;
         sel_z[i] = bv;
-        if ((be & 63) == lane) taken |= 1u << (be >> 6);
+        if ((be & 15) == sub) taken |= 1u << (be >> 4);
       }
     }
     // renormalised top-k gates
@@ -257,21 +328,28 @@ __global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
 
 #pragma unroll
     for (int i = 0; i < kMaxK; ++i) {
-      if (i < k && i == lane) {
+      if (tvalid && i < k && i == sub) {
         const size_t o = static_cast<size_t>(t) * k + i;
         const float gh = a.skip_disable ? gsel[i] : (kept[i] ? gsel[i] / zgate : 0.f);
         a.topk_idx[o] = sel_e[i];
         a.keep[o] = kept[i] ? 1 : 0;
         a.gates[o] = gh;
         if (a.scores) a.scores[o] = c[i];
-        if (kept[i]) {
-          atomicOr(&a.bitmap[static_cast<size_t>(sel_e[i]) * a.W + (t >> 6)], 1ull << (t & 63));
-        } else {
-          a.slot_row[o] = -1;
-        }
+        if (!kept[i]) a.slot_row[o] = -1;
+        my_e = sel_e[i];
+        my_kept = kept[i];
       }
     }
   }
+  // ---- 4. per-expert token masks of this workgroup -> local ranks and counts
+  if (my_kept) atomicOr(&emask[my_e], 1u << tl);
+  __syncthreads();
+  if (my_kept) {
+    const uint32_t below = emask[my_e] & ((1u << tl) - 1u);
+    a.local_rank[static_cast<size_t>(t) * k + sub] = static_cast<uint8_t>(__popc(below));
+  }
+  for (int e = tid; e < N; e += 256)
+    a.chunk_count[static_cast<size_t>(blockIdx.x) * N + e] = static_cast<uint8_t>(__popc(emask[e]));
 }
 
 template <typename T>
@@ -289,24 +367,10 @@ hipError_t launch_route_t(const RouteArgs &a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-__global__ void zero_u64_kernel(unsigned long long *p, size_t n) {
-  for (size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x; i < n;
-       i += static_cast<size_t>(gridDim.x) * blockDim.x)
-    p[i] = 0ull;
-}
-
 }  // namespace
 
 hipError_t launch_route(const RouteArgs &a, bool bf16, hipStream_t stream) {
   return bf16 ? launch_route_t<bf16_t>(a, stream) : launch_route_t<float>(a, stream);
-}
-
-hipError_t launch_zero_u64(unsigned long long *p, size_t n, hipStream_t stream) {
-  if (n == 0) return hipSuccess;
-  size_t blocks = (n + 255) / 256;
-  if (blocks > 1024) blocks = 1024;
-  zero_u64_kernel<<<dim3(static_cast<unsigned>(blocks)), 256, 0, stream>>>(p, n);
-  return hipGetLastError();
 }
 
 }  // namespace ace
