@@ -15,7 +15,7 @@
 // the layer streams every activated expert's weights once and is HBM-bound:
 //  * an M tile holds up to 256 rows, so an expert's weights are read once per
 //    tile (a 128-row tile would re-read them for every expert past 128 rows);
-//    the row count selects one of five unrolled bodies (32..256 rows) so MFMAs
+//    the row count selects one of four unrolled bodies (64..256 rows) so MFMAs
 //    and loads are issued only for the 16-row blocks a tile has;
 //  * operands move HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging)
 //    through two LDS rings: activations (L2-resident) 2-3 K stages deep, expert
@@ -25,7 +25,8 @@
 //  * one DMA instruction moves one MFMA fragment (16 rows x 32 k) and lane i
 //    lands at byte 16*i, which is exactly where lane i reads it back: LDS reads
 //    and writes are linear and bank-conflict free;
-//  * 4 waves as 2 x 2: a wave owns half the row blocks (interleaved, so short
+//  * 8 waves (two per SIMD, so one wave's LDS reads overlap the other's MFMAs)
+//    as 4 x 2: a wave owns a quarter of the row blocks (interleaved, so short
 //    tiles stay balanced) and two column groups (gate/up: gate and up blocks of
 //    the same 16 features, so SwiGLU happens in registers; down: 32 columns).
 // fp32 path: plain tiled FMA (small parity workloads).
@@ -42,8 +43,6 @@ namespace {
 constexpr int BK = 64;               // K per stage
 constexpr int kFragBytes = 1024;     // one MFMA fragment: 16 rows x 32 bf16
 constexpr int kLdsBytes = 144 * 1024;
-constexpr int GU_BN = 64;            // gate/up: intermediate features per tile
-constexpr int DN_BN = 128;           // down: output columns per tile
 
 struct TileInfo {
   int e, row0, rows;
@@ -116,48 +115,69 @@ __device__ __forceinline__ void wait_vmcnt(int n) {
 #undef ACE_VMCNT_CASE
 }
 
-// Pipeline geometry for a tile of MB 16-row blocks.  A (activation rows, mostly
-// L2 hits) and B (expert weights, streamed from HBM) have their own LDS rings:
-// A is prefetched SA-1 stages ahead, B SB-1 stages ahead, SB as deep as LDS
-// allows after the A ring.
-template <int MB> struct Pipe {
-  static constexpr int NA = MB / 2;                 // A DMAs per wave per stage
-  static constexpr int NB = 4;                      // B DMAs per wave per stage
+constexpr int kWaves = 8;  // waves per workgroup (two per SIMD)
+
+// Pipeline geometry for a tile of MB 16-row blocks (MB a multiple of 4) and CG
+// column groups (gate/up: 16 features each, a gate and an up block; down: 32
+// output columns, two blocks).  A (activation rows, mostly L2 hits) and B
+// (expert weights, streamed from HBM) have their own LDS rings within 144 KB.
+template <int MB, int CG> struct Pipe {
+  static constexpr int NA = MB / 4;                 // A DMAs per wave per stage (2*MB per workgroup)
+  static constexpr int NB = CG / 2;                 // B DMAs per wave per stage (4*CG per workgroup)
   static constexpr int ASZ = 2 * MB * kFragBytes;   // A stage: MB row blocks x 2 k halves
-  static constexpr int BSZ = 16 * kFragBytes;       // B stage: 8 column blocks x 2 k halves
-  static constexpr int SA = MB >= 12 ? 2 : 3;
+  static constexpr int BSZ = 4 * CG * kFragBytes;   // B stage: 2*CG column blocks x 2 k halves
+  static constexpr int SA = (MB >= 16 || (CG == 8 && MB >= 8)) ? 2 : MB >= 8 ? 3 : 4;
   static constexpr int SB0 = (kLdsBytes - SA * ASZ) / BSZ;
   static constexpr int SB = SB0 > 8 ? 8 : SB0;
-  static_assert(SB >= 3, "B ring too shallow");
-  static_assert(NB + NA + NB <= 31, "outstanding DMAs exceed the wait table");
+  static_assert(SB >= 2 && SA >= 2, "ring too shallow");
+  static_assert((SA - 1) * NA + (SB - 1) * NB + NA + NB <= 31, "outstanding DMAs exceed the wait table");
 };
 
-// DMAs this wave issued after the A part of stage kt, at the wait before stage
-// kt's compute.  Issue order: prologue B(0..SB-2), A(0..SA-2); then iteration j
-// (after its barrier) issues A(j+SA-1) and B(j+SB-1) when they exist.  vmcnt
-// completes in order, so once A(kt) is done, B(kt) (issued earlier) is too.
-template <int MB>
-__device__ __forceinline__ int ops_after_a(int kt, int nk) {
-  using P = Pipe<MB>;
-  int n = 0;
-  if (kt <= P::SA - 2)
-    n += max(0, min(P::SA - 1, nk) - 1 - kt) * P::NA;  // later prologue A stages that exist
-  else if (kt - P::SA + 1 + P::SB - 1 < nk)
-    n += P::NB;
-  for (int j = max(0, kt - P::SA + 2); j < kt; ++j)
-    n += (j + P::SA - 1 < nk ? P::NA : 0) + (j + P::SB - 1 < nk ? P::NB : 0);
-  return n;
+// This wave's DMA issue sequence: a prologue of B stages 0..PB-1 then A stages
+// 0..PA-1 (PB = min(SB-1, nk), PA = min(SA-1, nk)); then iteration j issues
+// A(j+SA-1) and then B(j+SB-1), each only if it exists.  cum_ops(j) = DMAs
+// issued before iteration j.
+template <class P>
+__device__ __forceinline__ int cum_ops(int j, int nk) {
+  const int PB = min(P::SB - 1, nk), PA = min(P::SA - 1, nk);
+  return PB * P::NB + PA * P::NA + max(0, min(j, nk - P::SA + 1)) * P::NA +
+         max(0, min(j, nk - P::SB + 1)) * P::NB;
 }
 
-// One M tile x one N tile with MB 16-row blocks (MB even, <= 16).
-// Waves form a 2 x 2 grid: wave (wr, wc) computes the interleaved row blocks
-// wr, wr+2, ... against column groups 2wc and 2wc+1 (gate/up: 16 features each,
-// as a gate block and an up block; down: 32 output columns each).
-template <bool GATEUP, int MB>
+// DMAs that may still be outstanding at the wait before stage kt's compute:
+// everything issued after the later of A(kt) and B(kt) (vmcnt completes in
+// issue order).
+template <class P>
+__device__ __forceinline__ int pending_ok(int kt, int nk) {
+  const int PB = min(P::SB - 1, nk), PA = min(P::SA - 1, nk);
+  int end_a, end_b;
+  if (kt < PA) {
+    end_a = PB * P::NB + (kt + 1) * P::NA;
+  } else {
+    end_a = cum_ops<P>(kt - P::SA + 1, nk) + P::NA;
+  }
+  if (kt < PB) {
+    end_b = (kt + 1) * P::NB;
+  } else {
+    const int i = kt - P::SB + 1;
+    end_b = cum_ops<P>(i, nk) + (i + P::SA - 1 < nk ? P::NA : 0) + P::NB;
+  }
+  return cum_ops<P>(kt, nk) - max(end_a, end_b);
+}
+
+// One M tile x one N tile with MB 16-row blocks and CG column groups.  The B
+// stage holds 4*CG fragments b = 4 fg + 2 cb + h: column group fg, block cb
+// (gate/up: cb 0 gate, 1 up; down: the group's two 16-column halves), k half h.
+// Wave w stages A fragments w, w+8, ... and B fragments w*NB .. w*NB+NB-1, and
+// computes row blocks wr, wr+4, ... (wr = w/2) against the CG/2 column groups
+// starting at wc*CG/2 (wc = w%2).
+template <bool GATEUP, int MB, int CG>
 __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, uint8_t *smem) {
-  using P = Pipe<MB>;
-  constexpr int NA = P::NA, SA = P::SA, SB = P::SB;
-  constexpr int MW = MB / 2;  // row blocks per wave
+  using P = Pipe<MB, CG>;
+  constexpr int NA = P::NA, NB = P::NB, SA = P::SA, SB = P::SB;
+  constexpr int MW = MB / 4;   // row blocks per wave
+  constexpr int CW = CG / 2;   // column groups per wave
+  constexpr int BN = GATEUP ? 16 * CG : 32 * CG;  // tile width (features or output columns)
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g = lane >> 4;
@@ -165,111 +185,111 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   const int K = GATEUP ? a.d : a.m;
   const bf16_t *act = static_cast<const bf16_t *>(a.act);
 
-  // A fragments this wave stages: f = wave + 4 j -> row block f / 2, k half f % 2
+  // A fragments this wave stages: f = wave + 8 j -> row block f / 2, k half f % 2
   const bf16_t *asrc[NA];
 #pragma unroll
   for (int j = 0; j < NA; ++j) {
-    const int f = wave + 4 * j;
+    const int f = wave + kWaves * j;
     const int row = min((f >> 1) * 16 + r16, ti.rows - 1);  // rows past the tile repeat its last row
     const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
     asrc[j] = act + static_cast<size_t>(src_row) * K + (f & 1) * 32 + 8 * g;
   }
-  // B fragments this wave stages: column group `wave` (two 16-column blocks x two k halves)
-  const bf16_t *bsrc[2];
-  if (GATEUP) {
-    const size_t f = static_cast<size_t>(ti.e) * a.m + nt * GU_BN + wave * 16 + r16;
-    bsrc[0] = static_cast<const bf16_t *>(a.w0) + f * a.d + 8 * g;
-    bsrc[1] = static_cast<const bf16_t *>(a.w1) + f * a.d + 8 * g;
-  } else {
-    const size_t n = static_cast<size_t>(ti.e) * a.d + nt * DN_BN + wave * 32 + r16;
-    bsrc[0] = static_cast<const bf16_t *>(a.w0) + n * a.m + 8 * g;
-    bsrc[1] = bsrc[0] + static_cast<size_t>(16) * a.m;
+  // B fragments this wave stages: b = wave * NB + t
+  const bf16_t *bsrc[NB];
+#pragma unroll
+  for (int t = 0; t < NB; ++t) {
+    const int b = wave * NB + t;
+    const int fg = b >> 2, cb = (b >> 1) & 1, h = b & 1;
+    if (GATEUP) {
+      const size_t f = static_cast<size_t>(ti.e) * a.m + nt * BN + fg * 16 + r16;
+      bsrc[t] = static_cast<const bf16_t *>(cb ? a.w1 : a.w0) + f * a.d + 32 * h + 8 * g;
+    } else {
+      const size_t n = static_cast<size_t>(ti.e) * a.d + nt * BN + fg * 32 + cb * 16 + r16;
+      bsrc[t] = static_cast<const bf16_t *>(a.w0) + n * a.m + 32 * h + 8 * g;
+    }
   }
   const uint32_t ldsA = lds_addr(smem);
   const uint32_t ldsB = ldsA + SA * P::ASZ;
   const uint8_t *smemA = smem;
   const uint8_t *smemB = smem + SA * P::ASZ;
 
-  f32x4_t acc[MW][4];
+  f32x4_t acc[MW][2 * CW];
 #pragma unroll
   for (int i = 0; i < MW; ++i)
 #pragma unroll
-    for (int c = 0; c < 4; ++c) acc[i][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < 2 * CW; ++c) acc[i][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nk = K / BK;
   // prologue: B stages 0..SB-2, then A stages 0..SA-2
   for (int s = 0; s < SB - 1 && s < nk; ++s) {
     const uint32_t st = ldsB + s * P::BSZ;
 #pragma unroll
-    for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) dma16(bsrc[cb] + s * BK + 32 * h, st + (wave * 4 + cb * 2 + h) * kFragBytes);
+    for (int t = 0; t < NB; ++t) dma16(bsrc[t] + s * BK, st + (wave * NB + t) * kFragBytes);
   }
   for (int s = 0; s < SA - 1 && s < nk; ++s) {
     const uint32_t st = ldsA + s * P::ASZ;
 #pragma unroll
-    for (int j = 0; j < NA; ++j) dma16(asrc[j] + s * BK, st + (wave + 4 * j) * kFragBytes);
+    for (int j = 0; j < NA; ++j) dma16(asrc[j] + s * BK, st + (wave + kWaves * j) * kFragBytes);
   }
 
   for (int kt = 0; kt < nk; ++kt) {
-    wait_vmcnt(ops_after_a<MB>(kt, nk));
+    wait_vmcnt(pending_ok<P>(kt, nk));
     barrier();  // stage kt landed for every wave; every wave is done with stage kt-1
     if (kt + SA - 1 < nk) {
       const int s = kt + SA - 1;
       const uint32_t st = ldsA + (s % SA) * P::ASZ;
 #pragma unroll
-      for (int j = 0; j < NA; ++j) dma16(asrc[j] + s * BK, st + (wave + 4 * j) * kFragBytes);
+      for (int j = 0; j < NA; ++j) dma16(asrc[j] + s * BK, st + (wave + kWaves * j) * kFragBytes);
     }
     if (kt + SB - 1 < nk) {
       const int s = kt + SB - 1;
       const uint32_t st = ldsB + (s % SB) * P::BSZ;
 #pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) dma16(bsrc[cb] + s * BK + 32 * h, st + (wave * 4 + cb * 2 + h) * kFragBytes);
+      for (int t = 0; t < NB; ++t) dma16(bsrc[t] + s * BK, st + (wave * NB + t) * kFragBytes);
     }
     const uint8_t *sa = smemA + (kt % SA) * P::ASZ;
     const uint8_t *sb = smemB + (kt % SB) * P::BSZ;
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
-      bf16x8_t b[4];  // [fl * 2 + cb]: column group 2wc + fl, block cb
+      bf16x8_t bf[2 * CW];  // [fl * 2 + cb]: column group wc*CW + fl, block cb
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        b[c] = *reinterpret_cast<const bf16x8_t *>(sb + ((2 * wc + (c >> 1)) * 4 + (c & 1) * 2 + h) * kFragBytes +
-                                                   16 * lane);
+      for (int c = 0; c < 2 * CW; ++c)
+        bf[c] = *reinterpret_cast<const bf16x8_t *>(sb + ((wc * CW + (c >> 1)) * 4 + (c & 1) * 2 + h) * kFragBytes +
+                                                    16 * lane);
 #pragma unroll
       for (int i = 0; i < MW; ++i) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t *>(sa + (2 * (2 * i + wr) + h) * kFragBytes + 16 * lane);
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t *>(sa + (2 * (wr + 4 * i) + h) * kFragBytes + 16 * lane);
 #pragma unroll
-        for (int c = 0; c < 4; ++c) acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, b[c], acc[i][c], 0, 0, 0);
+        for (int c = 0; c < 2 * CW; ++c)
+          acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bf[c], acc[i][c], 0, 0, 0);
       }
     }
   }
 
   // epilogue: lane holds column r16 of each block, rows 4*g + q
 #pragma unroll
-  for (int fl = 0; fl < 2; ++fl) {
-    const int grp = 2 * wc + fl;
+  for (int fl = 0; fl < CW; ++fl) {
+    const int grp = wc * CW + fl;
     if (GATEUP) {
       bf16_t *H = static_cast<bf16_t *>(a.out);
-      const int f = nt * GU_BN + grp * 16 + r16;
+      const int f = nt * BN + grp * 16 + r16;
 #pragma unroll
       for (int i = 0; i < MW; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int row = (2 * i + wr) * 16 + 4 * g + q;
+          const int row = (wr + 4 * i) * 16 + 4 * g + q;
           if (row < ti.rows)
             H[static_cast<size_t>(ti.row0 + row) * a.m + f] =
                 f32_to_bf16(silu(acc[i][fl * 2][q]) * acc[i][fl * 2 + 1][q]);
         }
     } else {
       bf16_t *Y = static_cast<bf16_t *>(a.out);
-      const int n = nt * DN_BN + grp * 32 + r16;
+      const int n = nt * BN + grp * 32 + r16;
 #pragma unroll
       for (int i = 0; i < MW; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int row = (2 * i + wr) * 16 + 4 * g + q;
+          const int row = (wr + 4 * i) * 16 + 4 * g + q;
           if (row < ti.rows) {
             bf16_t *yr = Y + static_cast<size_t>(ti.row0 + row) * a.d + n;
             yr[0] = f32_to_bf16(acc[i][fl * 2][q]);
@@ -280,25 +300,26 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   }
 }
 
-template <bool GATEUP>
-__global__ __launch_bounds__(256) void grouped_gemm_bf16_kernel(GemmArgs a) {
-  const int nN = GATEUP ? a.m / GU_BN : a.d / DN_BN;
+// tile width in features (gate/up) or output columns (down) for CG column groups
+template <bool GATEUP> constexpr int tile_width(int cg) { return GATEUP ? 16 * cg : 32 * cg; }
+
+template <bool GATEUP, int CG>
+__global__ __launch_bounds__(kWaves * 64) void grouped_gemm_bf16_kernel(GemmArgs a) {
+  const int nN = (GATEUP ? a.m : a.d) / tile_width<GATEUP>(CG);
   int grp, nt;
   map_block(blockIdx.x, nN, &grp, &nt);
   const TileInfo ti = tile_info(a, grp);
   if (!ti.valid) return;
   __shared__ __align__(16) uint8_t smem[kLdsBytes];
   const int blocks = (ti.rows + 15) >> 4;
-  if (blocks <= 2)
-    gemm_tile<GATEUP, 2>(a, ti, nt, smem);
-  else if (blocks <= 4)
-    gemm_tile<GATEUP, 4>(a, ti, nt, smem);
+  if (blocks <= 4)
+    gemm_tile<GATEUP, 4, CG>(a, ti, nt, smem);
   else if (blocks <= 8)
-    gemm_tile<GATEUP, 8>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 8, CG>(a, ti, nt, smem);
   else if (blocks <= 12)
-    gemm_tile<GATEUP, 12>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 12, CG>(a, ti, nt, smem);
   else
-    gemm_tile<GATEUP, 16>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 16, CG>(a, ti, nt, smem);
 }
 
 // ------------------------------------------------------------------ fp32 (tiled FMA)
@@ -410,7 +431,15 @@ unsigned grid_for(int max_groups, int nN) {
 hipError_t launch_gateup(const GemmArgs &a, bool bf16, hipStream_t stream) {
   if (a.max_groups <= 0) return hipSuccess;
   if (bf16)
-    grouped_gemm_bf16_kernel<true><<<dim3(grid_for(a.max_groups, a.m / GU_BN)), 256, 0, stream>>>(a);
+  {
+    // 128 features per tile when they divide m, else 64
+    if (a.m % tile_width<true>(8) == 0)
+      grouped_gemm_bf16_kernel<true, 8>
+          <<<dim3(grid_for(a.max_groups, a.m / tile_width<true>(8))), kWaves * 64, 0, stream>>>(a);
+    else
+      grouped_gemm_bf16_kernel<true, 4>
+          <<<dim3(grid_for(a.max_groups, a.m / tile_width<true>(4))), kWaves * 64, 0, stream>>>(a);
+  }
   else
     gateup_f32_kernel<<<dim3(grid_for(a.max_groups, a.m / F_BN)), 256, 0, stream>>>(a);
   return hipGetLastError();
@@ -419,7 +448,15 @@ hipError_t launch_gateup(const GemmArgs &a, bool bf16, hipStream_t stream) {
 hipError_t launch_down(const GemmArgs &a, bool bf16, hipStream_t stream) {
   if (a.max_groups <= 0) return hipSuccess;
   if (bf16)
-    grouped_gemm_bf16_kernel<false><<<dim3(grid_for(a.max_groups, a.d / DN_BN)), 256, 0, stream>>>(a);
+  {
+    // 256 output columns per tile when they divide d, else 128
+    if (a.d % tile_width<false>(8) == 0)
+      grouped_gemm_bf16_kernel<false, 8>
+          <<<dim3(grid_for(a.max_groups, a.d / tile_width<false>(8))), kWaves * 64, 0, stream>>>(a);
+    else
+      grouped_gemm_bf16_kernel<false, 4>
+          <<<dim3(grid_for(a.max_groups, a.d / tile_width<false>(4))), kWaves * 64, 0, stream>>>(a);
+  }
   else
     down_f32_kernel<<<dim3(grid_for(a.max_groups, a.d / F_BN)), 256, 0, stream>>>(a);
   return hipGetLastError();
