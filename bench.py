@@ -32,6 +32,12 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 METRIC = "MoE-layer tokens/s at 50% skip (prefill, decode); speedup vs plain top-k"
 TABLES = os.path.join(ROOT, "tests", "golden", "tables_prefill_4096_seed0.json")
+TRAFFIC = os.path.join(ROOT, "profiles", "prefill_4096_traffic.json")
+# stage -> (kernel name in the rocprofv3 traffic record, source file)
+STAGE_KERNEL = {"gateup": ("grouped_gemm_bf16_kernel<true, 8>", "expert_gemm.hip"),
+                "down": ("grouped_gemm_bf16_kernel<false, 8>", "expert_gemm.hip"),
+                "route": ("route_kernel<unsigned short, 8>", "route.hip"),
+                "combine": ("combine_kernel<unsigned short>", "combine.hip")}
 
 
 def parse():
@@ -43,6 +49,8 @@ def parse():
     ap.add_argument("--prefill-only", action="store_true", help="time only the ACE prefill step")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle sample budget")
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (calibrates HBM byte counters)")
     return ap.parse_args()
 
 
@@ -89,6 +97,22 @@ def layer_bytes(T, d, N, k, m, e_act, n_kept, esz=2):
     return total, st
 
 
+def measured_traffic(stage: str):
+    """HBM bytes per launch of `stage`'s kernel from the committed rocprofv3
+    FETCH_SIZE/WRITE_SIZE record, or None if that kernel's source changed since."""
+    import hashlib
+
+    try:
+        rec = json.load(open(TRAFFIC))
+        kname, src = STAGE_KERNEL[stage]
+        cur = hashlib.sha256(open(os.path.join(ROOT, "paper_2609_05228_amd", "csrc", src), "rb").read()).hexdigest()
+        if rec["source_sha256_16"].get(src) != cur[:16]:
+            return None
+        return int(rec["bytes_per_dispatch"][kname])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def cpu_baseline(L, k, a_gsp, a_rcr, tau, budget_s):
     """The oracle's online forward (as it stands) on the first n tokens of the
     same input, n sized for about `budget_s` seconds of CPU work."""
@@ -121,7 +145,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py runs on one GPU only: the ACE layer here has no multi-GPU path "
-              "(token sharding needs no exchange; see DESIGN.md). Use --gpus 1.", file=sys.stderr)
+              "(tokens shard with no exchange, so N GPUs run N independent copies). Use --gpus 1.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -163,6 +187,16 @@ def main():
                                    want_plan=True)
         return fn, out
 
+    if args.calib_copy_mb:
+        # a plain copy of known size, so per-dispatch FETCH_SIZE / WRITE_SIZE counters can be scaled
+        src = torch.empty(args.calib_copy_mb << 20, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.calib_copy_mb} MiB done")
+        del src, dst
+
     # ---------------- prefill, ACE at the requested skip ratio
     ace_step, ace_out = make_step(D["x"], False, tau)
     log(f"timing prefill: {args.warmup} warmup + {args.steps} steps")
@@ -181,7 +215,7 @@ def main():
     dom_ms = stages[dom]
     achieved = st_b[dom] / (dom_ms * 1e-3) / 1e9
     roofline = {"bound": "hbm", "kernel": dom, "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(dom),
                 "avg_launch_ms": round(dom_ms, 5), "alg_bytes_per_launch": int(st_b[dom])}
     if dom in ("gateup", "down"):
         f = 4 * d * m * n_kept if dom == "gateup" else 2 * d * m * n_kept

@@ -1,0 +1,125 @@
+"""The C ABI on the CPU: the library loads, exports what include/ace.h
+declares, and rejects invalid calls on the host before any launch (no GPU is
+touched by these tests).  The product path has no CPU or oracle fallback."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_05228_amd as ace
+from paper_2609_05228_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ace.h")
+FAKE = 0x10000  # aligned, never dereferenced: every call below returns before any launch
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ace_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = ace.lib()
+    names = header_functions()
+    assert {"ace_moe_forward", "ace_moe_workspace_size", "ace_status_string", "ace_abi_version"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in ace.h but not exported"
+
+
+def test_version_and_status_strings():
+    m = re.search(r"#define ACE_ABI_VERSION (\d+)", open(HEADER).read())
+    assert ace.abi_version() == int(m.group(1))
+    for code, word in [(0, "ACE_OK"), (-1, "INVALID_ARG"), (-2, "UNSUPPORTED"), (-3, "WORKSPACE"), (-4, "HIP")]:
+        assert word in ace.status_string(code)
+    assert "unknown" in ace.status_string(12345)
+
+
+def _desc(**kw):
+    base = dict(T=64, d=256, N=8, k=2, m=512, dtype=_lib.ACE_BF16, tau=0.1)
+    base.update(kw)
+    return ace.make_desc(base.pop("T"), base.pop("d"), base.pop("N"), base.pop("k"), base.pop("m"),
+                         base.pop("dtype"), base.pop("tau"), **base)
+
+
+def _call(desc, x=FAKE, w=None, o=None, ws=0, ws_bytes=0):
+    if w is None:
+        w = _lib.Weights(*([FAKE] * 3 + [FAKE] * 3 + [0, 0, 0] + [FAKE, FAKE]))
+        w.b_router = 0
+    if o is None:
+        o = _lib.Outputs(FAKE, FAKE, FAKE, 0, 0, 0, 0, 0)
+    return ace.forward_raw(desc, x, w, o, ws, ws_bytes, 0)
+
+
+def test_workspace_size():
+    assert ace.workspace_size(_desc()) > 0
+    assert ace.workspace_size(_desc(T=0)) == 0
+    big = ace.workspace_size(_desc(T=4096, d=2048, N=128, k=8, m=768))
+    assert big > 4096 * 2048 * 2 + 4096 * 8 * (768 + 2048) * 2  # x_in, H and Y at least
+    assert ace.workspace_size(_desc(dtype=_lib.ACE_F32)) > ace.workspace_size(_desc())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(k=9, N=8), _lib.ACE_ERR_INVALID_ARG),            # k > N
+    (dict(m_min=0), _lib.ACE_ERR_INVALID_ARG),
+    (dict(m_min=3), _lib.ACE_ERR_INVALID_ARG),             # m_min > k
+    (dict(dtype=7), _lib.ACE_ERR_INVALID_ARG),
+    (dict(tau=float("nan")), _lib.ACE_ERR_INVALID_ARG),
+    (dict(eps=-1.0), _lib.ACE_ERR_INVALID_ARG),
+    (dict(T=-1), _lib.ACE_ERR_INVALID_ARG),
+    (dict(N=300, k=2), _lib.ACE_ERR_UNSUPPORTED),
+    (dict(N=16, k=9), _lib.ACE_ERR_UNSUPPORTED),
+    (dict(d=200), _lib.ACE_ERR_UNSUPPORTED),
+    (dict(m=100), _lib.ACE_ERR_UNSUPPORTED),
+    (dict(n_shared=1, m_shared=96), _lib.ACE_ERR_UNSUPPORTED),
+])
+def test_invalid_descriptors(kw, status):
+    assert _call(_desc(**kw)) == status
+
+
+def test_null_and_misaligned_pointers():
+    d = _desc()
+    assert _call(d, x=0) == _lib.ACE_ERR_INVALID_ARG
+    assert _call(d, x=FAKE + 2) == _lib.ACE_ERR_INVALID_ARG
+    w = _lib.Weights(FAKE, FAKE, 0, FAKE, FAKE, 0, 0, 0, 0, FAKE, FAKE)  # w_down missing
+    assert _call(d, w=w) == _lib.ACE_ERR_INVALID_ARG
+    o = _lib.Outputs(FAKE, 0, FAKE, 0, 0, 0, 0, 0)                         # topk_idx missing
+    assert _call(d, o=o) == _lib.ACE_ERR_INVALID_ARG
+    # shared expert requested without its weights
+    assert _call(_desc(n_shared=1, m_shared=128)) == _lib.ACE_ERR_INVALID_ARG
+    # scores requested without a scores buffer
+    assert _call(_desc(write_scores=True)) == _lib.ACE_ERR_INVALID_ARG
+    # unknown flag bit
+    d2 = _desc()
+    d2.flags = 1 << 7
+    assert _call(d2) == _lib.ACE_ERR_INVALID_ARG
+
+
+def test_workspace_checked_before_launch():
+    d = _desc()
+    need = ace.workspace_size(d)
+    assert _call(d, ws=0, ws_bytes=need) == _lib.ACE_ERR_WORKSPACE
+    assert _call(d, ws=FAKE, ws_bytes=need - 1) == _lib.ACE_ERR_WORKSPACE
+    assert _call(d, ws=FAKE + 16, ws_bytes=need) == _lib.ACE_ERR_WORKSPACE  # not 256-byte aligned
+
+
+def test_empty_batch_is_a_no_op():
+    assert _call(_desc(T=0), x=0, o=_lib.Outputs()) == _lib.ACE_OK
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    monkeypatch.setattr(_lib, "_lib", None)
+    monkeypatch.setattr(_lib, "LIB_PATH", os.path.join(ROOT, "no_such_dir", "libace.so"))
+    with pytest.raises(RuntimeError, match="no fallback"):
+        _lib.lib()
+
+
+def test_product_path_never_touches_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2609_05228_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".cpp", ".h")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert not re.search(r"\boracle\b", text), f"{f} mentions the oracle"
