@@ -36,8 +36,19 @@ TRAFFIC = os.path.join(ROOT, "profiles", "prefill_4096_traffic.json")
 # stage -> (kernel name in the rocprofv3 traffic record, source file)
 STAGE_KERNEL = {"gateup": ("grouped_gemm_bf16_kernel<true, 8>", "expert_gemm.hip"),
                 "down": ("grouped_gemm_bf16_kernel<false, 8>", "expert_gemm.hip"),
-                "route": ("route_kernel<unsigned short, 8>", "route.hip"),
+                "route": ("route_kernel<unsigned short, 8, false>", "route.hip"),
                 "combine": ("combine_kernel<unsigned short>", "combine.hip")}
+
+
+def source_digest(src: str) -> str:
+    """First 16 hex digits of sha256 over a kernel's source file and the
+    shared header it includes: the key that ties a traffic record to the code."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in (src, "ace_internal.h"):
+        h.update(open(os.path.join(ROOT, "paper_2609_05228_amd", "csrc", f), "rb").read())
+    return h.hexdigest()[:16]
 
 
 def parse():
@@ -100,13 +111,10 @@ def layer_bytes(T, d, N, k, m, e_act, n_kept, esz=2):
 def measured_traffic(stage: str):
     """HBM bytes per launch of `stage`'s kernel from the committed rocprofv3
     FETCH_SIZE/WRITE_SIZE record, or None if that kernel's source changed since."""
-    import hashlib
-
     try:
         rec = json.load(open(TRAFFIC))
         kname, src = STAGE_KERNEL[stage]
-        cur = hashlib.sha256(open(os.path.join(ROOT, "paper_2609_05228_amd", "csrc", src), "rb").read()).hexdigest()
-        if rec["source_sha256_16"].get(src) != cur[:16]:
+        if rec["source_sha256_16"].get(src) != source_digest(src):
             return None
         return int(rec["bytes_per_dispatch"][kname])
     except (OSError, KeyError, ValueError):

@@ -17,10 +17,18 @@ __device__ __forceinline__ float bf16_to_f32(bf16_t b) {
 }
 
 // round to nearest, ties to even (inputs here are finite)
+typedef __bf16 bf16x2_hw_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_hw_t __attribute__((ext_vector_type(2)));
+
+// two fp32 -> two bf16 packed in one dword (lo in bits 0-15), round to
+// nearest even, one v_cvt_pk_bf16_f32
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  const f32x2_hw_t v = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_hw_t));
+}
+
 __device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<bf16_t>(u >> 16);
+  return static_cast<bf16_t>(pack_bf16x2(f, 0.f) & 0xFFFFu);
 }
 
 template <typename T> struct Elem;
@@ -39,6 +47,13 @@ constexpr int kMaxN = 256;   // routed experts supported by the router kernel
 constexpr int kMaxK = 8;     // top-k supported by the router kernel
 constexpr int kTileM = 256;  // rows of one grouped-GEMM M tile (the dispatch plan's tile size)
 constexpr int kRouteTokens = 16;  // tokens per router workgroup (one dispatch-plan chunk)
+constexpr int kRouteMaxSlices = 16;  // K slices of the small-batch router
+
+// 16-expert tiles the router kernels are compiled for: 1, 2, 4, 8 or 16 (>= N / 16)
+inline int route_expert_tiles(int N) {
+  const int need = (N + 15) / 16;
+  return need <= 1 ? 1 : need <= 2 ? 2 : need <= 4 ? 4 : need <= 8 ? 8 : 16;
+}
 
 // ---------------------------------------------------------------- kernel arguments
 struct RouteArgs {
@@ -56,6 +71,10 @@ struct RouteArgs {
   int32_t *slot_row;      // [T, k]: -1 for skipped slots (kept slots are filled by the plan)
   uint8_t *local_rank;    // [T, k]: rank of a kept slot among its chunk's kept slots of that expert
   uint8_t *chunk_count;   // [G, N]: kept slots per (16-token chunk, expert)
+  float *zpart;           // [ksplit, T, zstride]: partial logits of the K slices (ksplit > 0)
+  float *sspart;          // [ksplit, T]: partial sums of squares of x
+  int ksplit;             // 0: one fused kernel; else K slices (<= 16, dividing d / 32)
+  int zstride;            // 16 * route_expert_tiles(N)
   int T, d, N, k, m_min;
   float tau, eps, rms_eps;
   int skip_disable;
@@ -94,8 +113,20 @@ struct GemmArgs {
   int d, m;               // hidden and intermediate sizes of this GEMM's expert(s)
 };
 
+// Small-batch (decode) grouped GEMM: the same tiles, split over K into
+// `splits` parts when the batch is too small to fill the GPU otherwise.
+struct SkinnyArgs {
+  GemmArgs g;
+  int splits;      // K splits (1: write H / Y in bf16 directly)
+  int rows_cap;    // row capacity of a partial-sum plane (T * k)
+  float *part0;    // gate/up: gate partials [splits, rows_cap, m]; down: Y partials [splits, rows_cap, d]
+  float *part1;    // gate/up: up partials [splits, rows_cap, m]
+};
+
 struct CombineArgs {
-  const void *Y;          // [rows, d] routed expert outputs in compacted order
+  const void *Y;          // [rows, d] routed expert outputs in compacted order, or null
+  const float *Ypart;     // [ysplits, rows_cap, d] fp32 partial sums of Y, or null
+  int ysplits, rows_cap;
   const void *Ys;         // [T, d] shared-expert output, or null
   const int32_t *slot_row;  // [T, k]
   const float *gates;       // [T, k]
@@ -110,5 +141,8 @@ hipError_t launch_plan(const PlanArgs &a, hipStream_t stream);
 hipError_t launch_gateup(const GemmArgs &a, bool bf16, hipStream_t stream);
 hipError_t launch_down(const GemmArgs &a, bool bf16, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs &a, bool bf16, hipStream_t stream);
+// gate/up (gateup = true; reduces K-split partials into H when splits > 1, with
+// n_rows = device count of rows in routed mode) or down
+hipError_t launch_skinny(const SkinnyArgs &a, bool gateup, const int32_t *n_rows, hipStream_t stream);
 
 }  // namespace ace

@@ -21,10 +21,26 @@ constexpr size_t kAlign = 256;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
+constexpr int kSkinnyMaxT = 64;      // batches up to this many tokens take the small-batch GEMMs
+constexpr long kSkinnyWaves = 4096;  // K-split until about this many waves stream weights
+
+// K splits for the small-batch GEMMs: double while the work items stay under
+// kSkinnyWaves and each split keeps a whole number of >= 2 64-wide K steps
+int pick_splits(long items, int K) {
+  int s = 1;
+  while (s < 8 && items * s * 2 <= kSkinnyWaves && (K / (2 * s)) % 64 == 0 && K / (2 * s) >= 128 &&
+         K % (2 * s) == 0)
+    s *= 2;
+  return s;
+}
+
 struct Layout {
-  size_t xn, local_rank, chunk_count, chunk_base, slot_row, gates, counts, offsets, perm;
-  size_t tile_e, tile_r0, tile_rows, n_tiles, H, Y, Hs, Ys, total;
+  size_t xn, zpart, sspart, local_rank, chunk_count, chunk_base, slot_row, gates, counts, offsets, perm;
+  size_t tile_e, tile_r0, tile_rows, n_tiles, H, Y, Hs, Ys, part_g, part_u, part_y, total;
   int G, max_groups, dense_groups;
+  bool skinny;          // small-batch path (bf16, T <= kSkinnyMaxT)
+  int splits_gu, splits_dn;
+  int ksplit, zstride;  // router K slices (0: fused) and partial-logit row stride
 };
 
 Layout layout_for(const ace_moe_desc &d) {
@@ -34,6 +50,21 @@ Layout layout_for(const ace_moe_desc &d) {
   const size_t esz = (d.dtype == ACE_BF16) ? 2 : 4;
   const size_t slots = T * k;
   L.G = static_cast<int>((T + ace::kRouteTokens - 1) / ace::kRouteTokens);
+  // router: small batches spread W_r over (chunk, K slice) workgroups
+  L.ksplit = 0;
+  if (L.G <= 16) {
+    const int nb = d.d / 32;
+    L.ksplit = 1;
+    while (L.ksplit < ace::kRouteMaxSlices && nb % (2 * L.ksplit) == 0 && L.G * L.ksplit < 128) L.ksplit *= 2;
+  }
+  L.zstride = 16 * ace::route_expert_tiles(d.N);
+  L.skinny = d.dtype == ACE_BF16 && d.T <= kSkinnyMaxT;
+  L.splits_gu = L.splits_dn = 1;
+  if (L.skinny) {
+    const long tiles = static_cast<long>(slots < N ? slots : N);
+    L.splits_gu = pick_splits(tiles * (d.m / 16), d.d);
+    L.splits_dn = pick_splits(tiles * (d.d / 32), d.m);
+  }
   L.max_groups = static_cast<int>((slots + ace::kTileM - 1) / ace::kTileM + (slots < N ? slots : N));
   L.dense_groups = static_cast<int>((T + ace::kTileM - 1) / ace::kTileM);
   size_t off = 0;
@@ -43,6 +74,8 @@ Layout layout_for(const ace_moe_desc &d) {
     return o;
   };
   L.xn = take(T * dd * esz);
+  L.zpart = take(static_cast<size_t>(L.ksplit) * T * L.zstride * 4);
+  L.sspart = take(static_cast<size_t>(L.ksplit) * T * 4);
   L.local_rank = take(slots);
   L.chunk_count = take(static_cast<size_t>(L.G) * N);
   L.chunk_base = take(static_cast<size_t>(L.G) * N * 4);
@@ -61,6 +94,11 @@ Layout layout_for(const ace_moe_desc &d) {
     L.Hs = take(T * static_cast<size_t>(d.m_shared) * esz);
     L.Ys = take(T * dd * esz);
   }
+  if (L.splits_gu > 1) {
+    L.part_g = take(static_cast<size_t>(L.splits_gu) * slots * m * 4);
+    L.part_u = take(static_cast<size_t>(L.splits_gu) * slots * m * 4);
+  }
+  if (L.splits_dn > 1) L.part_y = take(static_cast<size_t>(L.splits_dn) * slots * dd * 4);
   L.total = off;
   return L;
 }
@@ -240,6 +278,10 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   ra.slot_row = slot_row;
   ra.local_rank = local_rank;
   ra.chunk_count = chunk_count;
+  ra.zpart = static_cast<float *>(at(L.zpart));
+  ra.sspart = static_cast<float *>(at(L.sspart));
+  ra.ksplit = L.ksplit;
+  ra.zstride = L.zstride;
   ra.T = d.T;
   ra.d = d.d;
   ra.N = d.N;
@@ -287,16 +329,24 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   g.max_groups = L.max_groups;
   g.d = d.d;
   g.m = d.m;
-  if (ace::launch_gateup(g, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
-  mark(prof, 3, stream);
-
   ace::GemmArgs gd = g;
   gd.act = at(L.H);
   gd.perm = nullptr;
   gd.w0 = w->w_down;
   gd.w1 = nullptr;
   gd.out = at(L.Y);
-  if (ace::launch_down(gd, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+  if (L.skinny) {
+    const int slots = d.T * d.k;
+    ace::SkinnyArgs su{g, L.splits_gu, slots, static_cast<float *>(at(L.part_g)), static_cast<float *>(at(L.part_u))};
+    if (ace::launch_skinny(su, true, offsets + d.N, stream) != hipSuccess) return ACE_ERR_HIP;
+    mark(prof, 3, stream);
+    ace::SkinnyArgs sd{gd, L.splits_dn, slots, static_cast<float *>(at(L.part_y)), nullptr};
+    if (ace::launch_skinny(sd, false, offsets + d.N, stream) != hipSuccess) return ACE_ERR_HIP;
+  } else {
+    if (ace::launch_gateup(g, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+    mark(prof, 3, stream);
+    if (ace::launch_down(gd, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+  }
   mark(prof, 4, stream);
 
   const void *Ys = nullptr;
@@ -311,19 +361,29 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
     s.max_groups = L.dense_groups;
     s.d = d.d;
     s.m = d.m_shared;
-    if (ace::launch_gateup(s, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
     ace::GemmArgs sd = s;
     sd.act = at(L.Hs);
     sd.w0 = w->ws_down;
     sd.w1 = nullptr;
     sd.out = at(L.Ys);
-    if (ace::launch_down(sd, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+    if (L.skinny) {
+      ace::SkinnyArgs su{s, 1, d.T, nullptr, nullptr};
+      ace::SkinnyArgs sdn{sd, 1, d.T, nullptr, nullptr};
+      if (ace::launch_skinny(su, true, nullptr, stream) != hipSuccess) return ACE_ERR_HIP;
+      if (ace::launch_skinny(sdn, false, nullptr, stream) != hipSuccess) return ACE_ERR_HIP;
+    } else {
+      if (ace::launch_gateup(s, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+      if (ace::launch_down(sd, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
+    }
     Ys = at(L.Ys);
   }
   mark(prof, 5, stream);
 
   ace::CombineArgs c{};
   c.Y = at(L.Y);
+  c.Ypart = L.splits_dn > 1 ? static_cast<const float *>(at(L.part_y)) : nullptr;
+  c.ysplits = L.splits_dn;
+  c.rows_cap = d.T * d.k;
   c.Ys = Ys;
   c.slot_row = slot_row;
   c.gates = gates;

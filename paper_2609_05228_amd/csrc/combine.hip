@@ -1,5 +1,7 @@
 // Gate-weighted combine of the sparsified MoE output (Eq. ace_sparse_output):
 //   y_t = sum_{i in I_t} ghat_{t,i} Y[slot_row[t,i]]  (+ the shared expert's row)
+// where Y rows are either bf16/fp32 rows or, after a K-split small-batch down
+// GEMM, the fp32 sum of their partials (added in split order).
 // One workgroup per token, 16-byte vectors across the hidden dimension, slots
 // added in slot order with fp32 FMA: deterministic, no atomics.
 #include "ace_internal.h"
@@ -21,11 +23,8 @@ template <> struct V<bf16_t> {
     }
   }
   static __device__ __forceinline__ void store(bf16_t *p, const float v[8]) {
-    uint32_t w[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      w[j] = static_cast<uint32_t>(f32_to_bf16(v[2 * j])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * j + 1])) << 16);
-    *reinterpret_cast<uint4 *>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+    *reinterpret_cast<uint4 *>(p) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                               pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
   }
 };
 template <> struct V<float> {
@@ -61,7 +60,24 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
       const int r = rows[i];
       if (r < 0) continue;
       float v[VN];
-      V<T>::load(Y + static_cast<size_t>(r) * a.d + c, v);
+      if (a.Ypart) {
+        // K-split partial sums of this row, added in split order
+#pragma unroll
+        for (int j = 0; j < VN; ++j) v[j] = 0.f;
+        for (int s = 0; s < a.ysplits; ++s) {
+          const float *p = a.Ypart + (static_cast<size_t>(s) * a.rows_cap + r) * a.d + c;
+#pragma unroll
+          for (int j = 0; j < VN; j += 4) {
+            const float4 q = *reinterpret_cast<const float4 *>(p + j);
+            v[j] += q.x;
+            v[j + 1] += q.y;
+            v[j + 2] += q.z;
+            v[j + 3] += q.w;
+          }
+        }
+      } else {
+        V<T>::load(Y + static_cast<size_t>(r) * a.d + c, v);
+      }
       const float g = gs[i];
 #pragma unroll
       for (int j = 0; j < VN; ++j) acc[j] = fmaf(g, v[j], acc[j]);

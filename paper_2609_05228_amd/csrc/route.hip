@@ -2,35 +2,42 @@
 // renormalisation, and the per-token ACE skipping of Alg. 4 (dual-view scores,
 // max fusion, top-1 and minimum-active safeguards, gate renormalisation).
 //
-// One workgroup (4 waves) owns 16 tokens.
-//  1. Each wave computes the RMS scale of 4 tokens (fp32 sum of squares).
-//  2. Router logits z = x_in W_r^T (App. B.2, Eq. app_router_logit) on fp32 MFMA
-//     (v_mfma_f32_16x16x4f32): x_in is the un-rounded fp32 RMSNorm output, so the
-//     top-k and skip decisions see fp32 logits, not bf16-rounded activations.
-//     Wave w owns a quarter of the hidden dimension and keeps two accumulator
-//     sets (alternating 32-wide K blocks); the 8 partial sums per logit are added
-//     in a fixed order, which keeps the accumulated rounding near 2e-7 for
-//     d = 2048.  The same pass writes x_in, rounded to the GEMM dtype, for the
-//     expert GEMMs.
-//     The hidden dimension is walked in 32-wide blocks (16-byte loads per lane)
-//     with the next block's operands loaded before the current block's MFMAs.
-//  3. Each 16-lane group of a wave takes one token (4 tokens per wave at once):
-//     top-k by k rounds of a 16-lane arg-max (ties go to the lower expert id),
-//     gates g = exp(z_i - z_1) / sum_j exp(z_j - z_1) over the k selected logits
-//     (the softmax over all N experts cancels in the renormalised gate), then
-//     Alg. 4 evaluated redundantly in every lane of the group (k <= 8 scalars),
-//     and lane i < k of the group writes slot i.
-//  4. For the dispatch plan, each kept slot gets its rank among this
-//     workgroup's kept slots of the same expert in token order (from a 16-bit
-//     token mask per expert in LDS), and the workgroup writes its per-expert
-//     kept counts.  No global atomics: the plan is independent of scheduling.
+// Per 16-token chunk (one dispatch-plan chunk):
+//  1. Logits.  z[t][e] = rstd_t * sum_k (x[t,k] gamma[k]) W_r[e,k] + b[e]
+//     (Sec. 3.1 x = x_bar Gamma; App. B.2, Eq. app_router_logit) with the RMS
+//     scale factored out of the sum.  K is cut into 32-wide blocks; a wave
+//     accumulates its blocks for 16 tokens x all N experts in MFMA
+//     accumulators, plus the per-token sum of squares of x.
+//       bf16: x and gamma are bf16, so x*gamma has at most 16 significant bits
+//       and splits exactly into hi + lo, both bf16; the logits take two
+//       v_mfma_f32_16x16x32_bf16 per 32 K (hi, then lo) against the bf16
+//       router rows, i.e. exact products accumulated in fp32, as an fp32 GEMM
+//       would, at bf16 matrix-core rate.
+//       fp32: v_mfma_f32_16x16x4f32 on the fp32 products.
+//     Partial sums are always added in a fixed order (wave order in LDS, then
+//     slice order), so results do not depend on scheduling.  The top-k and
+//     skip decisions never see bf16-rounded activations.
+//     A CU keeps only a few tens of KB of loads in flight, so one workgroup
+//     reading all of W_r is latency-bound.  Large batches (> 16 chunks) run one
+//     fused workgroup of 8 waves per chunk (every CU busy anyway); small
+//     batches first spread W_r over (chunk, K slice) workgroups that write
+//     partial logits, and the per-chunk kernel adds the slices.
+//  2. Selection (waves 0-3, one token per 16-lane group, lane i holds slot i):
+//     top-k by k rounds of a 16-lane arg-max on DPP row rotations (ties go to
+//     the lower expert id), gates g = exp(z_i - z_1) / sum_j exp(z_j - z_1)
+//     over the k selected logits (the softmax over all N experts cancels in
+//     the renormalised gate), then Alg. 4 with 16-lane sums.  For the dispatch
+//     plan each kept slot gets its rank among this chunk's kept slots of the
+//     same expert in token order (from a 16-bit token mask per expert in LDS)
+//     and the chunk's per-expert counts are written; no global atomics.
+//     Meanwhile waves 4-7 write x_in = x * rstd * gamma in the GEMM dtype.
 #include "ace_internal.h"
 
 namespace ace {
 
 namespace {
 
-constexpr int kTok = kRouteTokens;  // tokens per workgroup
+constexpr int kTok = kRouteTokens;  // tokens per router workgroup / plan chunk
 
 // 8 consecutive elements: raw storage and conversion
 template <typename T> struct Oct;
@@ -65,305 +72,460 @@ template <> struct Oct<bf16_t> {
     }
   }
   static __device__ __forceinline__ void store(bf16_t *p, const float v[8]) {
-    uint32_t w[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      w[j] = static_cast<uint32_t>(f32_to_bf16(v[2 * j])) | (static_cast<uint32_t>(f32_to_bf16(v[2 * j + 1])) << 16);
-    *reinterpret_cast<uint4 *>(p) = make_uint4(w[0], w[1], w[2], w[3]);
+    *reinterpret_cast<uint4 *>(p) = make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]),
+                                               pack_bf16x2(v[4], v[5]), pack_bf16x2(v[6], v[7]));
   }
 };
 
-template <typename T>
-__device__ __forceinline__ void load4(const T *p, float v[4]);
-template <>
-__device__ __forceinline__ void load4<float>(const float *p, float v[4]) {
-  const float4 q = *reinterpret_cast<const float4 *>(p);
-  v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+
+constexpr int kWaves = 8;
+
+// value of the lane n places further round this lane's 16-lane row (DPP row_ror)
+template <int n> __device__ __forceinline__ int row_ror(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, 0x120 + n, 0xF, 0xF, false);
 }
-template <>
-__device__ __forceinline__ void load4<bf16_t>(const bf16_t *p, float v[4]) {
-  const uint2 q = *reinterpret_cast<const uint2 *>(p);
-  v[0] = __uint_as_float(q.x << 16);
-  v[1] = __uint_as_float(q.x & 0xFFFF0000u);
-  v[2] = __uint_as_float(q.y << 16);
-  v[3] = __uint_as_float(q.y & 0xFFFF0000u);
+template <int n> __device__ __forceinline__ float row_ror(float v) {
+  return __int_as_float(row_ror<n>(__float_as_int(v)));
 }
 
-__device__ __forceinline__ bool better(float v, int e, float bv, int be) {
-  return v > bv || (v == bv && e < be);
+// sum over the 16-lane row; a + b == b + a, so every lane ends with the same bits
+__device__ __forceinline__ float group_sum(float v) {
+  v += row_ror<8>(v);
+  v += row_ror<4>(v);
+  v += row_ror<2>(v);
+  v += row_ror<1>(v);
+  return v;
 }
 
-// Operands of one 32-wide K block for one lane: the lane's 8 consecutive k of
-// its token row, of gamma and of NT router rows.  MFMA j of the block takes
-// element j from every lane, so lane group g supplies k = kb + 8g + j to both
-// operands and the block covers kb .. kb + 31.
-template <typename T, int NT> struct Block {
+// Top-k keys: (logit, expert) as one 64-bit integer whose order is the
+// selection order (larger logit first, then lower expert id); 0 = no candidate.
+__device__ __forceinline__ uint64_t topk_key(float z, int e) {
+  uint32_t u = __float_as_uint(z + 0.0f);  // -0 -> +0, so equal logits tie on the expert id
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (static_cast<uint64_t>(u) << 32) | static_cast<uint32_t>(~e);
+}
+__device__ __forceinline__ float key_logit(uint64_t key) {
+  const uint32_t u = static_cast<uint32_t>(key >> 32);
+  return __uint_as_float((u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u);
+}
+__device__ __forceinline__ int key_expert(uint64_t key) { return static_cast<int>(~static_cast<uint32_t>(key)); }
+
+template <int n> __device__ __forceinline__ uint64_t row_ror64(uint64_t v) {
+  const uint32_t lo = static_cast<uint32_t>(row_ror<n>(static_cast<int>(static_cast<uint32_t>(v))));
+  const uint32_t hi = static_cast<uint32_t>(row_ror<n>(static_cast<int>(static_cast<uint32_t>(v >> 32))));
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+// maximum over the 16-lane row, in every lane
+__device__ __forceinline__ uint64_t row_max64(uint64_t v) {
+  uint64_t o = row_ror64<8>(v);
+  v = o > v ? o : v;
+  o = row_ror64<4>(v);
+  v = o > v ? o : v;
+  o = row_ror64<2>(v);
+  v = o > v ? o : v;
+  o = row_ror64<1>(v);
+  return o > v ? o : v;
+}
+
+// bitonic sort, descending, of n (a power of two) keys in registers
+template <int n> __device__ __forceinline__ void sort_desc(uint64_t (&a)[n]) {
+#pragma unroll
+  for (int blk = 2; blk <= n; blk <<= 1)
+#pragma unroll
+    for (int j = blk >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < n; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          const uint64_t x = a[i], y = a[l];
+          const bool sw = ((i & blk) == 0) ? (x < y) : (x > y);
+          a[i] = sw ? y : x;
+          a[l] = sw ? x : y;
+        }
+      }
+}
+
+// number of lanes of this 16-lane group with b set
+__device__ __forceinline__ int group_count(bool b) {
+  const unsigned long long m = __ballot(b);
+  return __popcll((m >> (threadIdx.x & 48)) & 0xFFFFull);
+}
+
+// One 32-wide K block of a lane: its 8 consecutive k of the token row, of gamma
+// and of the router row of each of its NT experts (expert 16 f + lane % 16).
+// Lane group g = lane / 16 supplies k = 32 j + 8 g + i (i = 0..7) to both MFMA
+// operands: the A/B fragment layout of v_mfma_f32_16x16x32_bf16, and for
+// v_mfma_f32_16x16x4f32 instruction i takes element i of every lane.
+template <typename T, int NT> struct Stage {
   typename Oct<T>::raw x, g, w[NT];
 };
 
 template <typename T, int NT>
-__device__ __forceinline__ void load_block(Block<T, NT> &b, const T *xrow, const T *gamma, const T *wr,
-                                           int d, int N, int r16, int k) {
-  b.x = Oct<T>::load(xrow + k);
-  b.g = Oct<T>::load(gamma + k);
+__device__ __forceinline__ void load_stage(Stage<T, NT> &st, const T *xrow, const T *gl, const T *wl,
+                                           const int (&woff)[NT], int k) {
+  st.x = Oct<T>::load(xrow + k);
+  st.g = Oct<T>::load(gl + k);
 #pragma unroll
-  for (int et = 0; et < NT; ++et) {
-    const int e = min(et * 16 + r16, N - 1);  // rows past N reuse row N-1; their logits are never read
-    b.w[et] = Oct<T>::load(wr + static_cast<size_t>(e) * d + k);
-  }
+  for (int f = 0; f < NT; ++f) st.w[f] = Oct<T>::load(wl + woff[f] + k);
 }
 
-template <typename T, int NT>
-__device__ __forceinline__ void mfma_block(const Block<T, NT> &b, f32x4_t (&acc)[NT], float rs, bool tvalid,
-                                           T *xnp) {
-  float xv[8], gv[8], av[8];
-  Oct<T>::cvt(b.x, xv);
-  Oct<T>::cvt(b.g, gv);
+// live = false: the stage holds a clamped (already counted) block; its
+// activations are taken as zero so the MFMAs need no branch
+template <int NT>
+__device__ __forceinline__ void mma_stage(const Stage<bf16_t, NT> &st, f32x4_t (&acc)[NT], float &ss, bool live) {
+  float xv[8], gv[8];
+  const uint4 xr = live ? st.x : make_uint4(0u, 0u, 0u, 0u);
+  Oct<bf16_t>::cvt(xr, xv);
+  Oct<bf16_t>::cvt(st.g, gv);
+  uint32_t hi[4], lo[4];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) av[j] = tvalid ? (xv[j] * rs) * gv[j] : 0.f;
-  if (tvalid) Oct<T>::store(xnp, av);
+  for (int q = 0; q < 4; ++q) {
+    uint32_t h[2], l[2];
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-#pragma unroll
-    for (int et = 0; et < NT; ++et) {
-      float bv[8];
-      Oct<T>::cvt(b.w[et], bv);
-      acc[et] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[j], bv[j], acc[et], 0, 0, 0);
+    for (int u = 0; u < 2; ++u) {
+      const float xe = xv[2 * q + u];
+      ss = fmaf(xe, xe, ss);
+      const float p = xe * gv[2 * q + u];  // exact: two 8-bit significands
+      const uint32_t pb = __float_as_uint(p) & 0xFFFF0000u;
+      h[u] = pb;
+      l[u] = __float_as_uint(p - __uint_as_float(pb));  // exact, <= 8 significant bits
     }
+    hi[q] = (h[0] >> 16) | h[1];
+    lo[q] = (l[0] >> 16) | (l[1] & 0xFFFF0000u);
+  }
+  const bf16x8_t ahi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+  const bf16x8_t alo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+#pragma unroll
+  for (int f = 0; f < NT; ++f)
+    acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, __builtin_bit_cast(bf16x8_t, st.w[f]), acc[f], 0, 0, 0);
+#pragma unroll
+  for (int f = 0; f < NT; ++f)
+    acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, __builtin_bit_cast(bf16x8_t, st.w[f]), acc[f], 0, 0, 0);
+}
+
+template <int NT>
+__device__ __forceinline__ void mma_stage(const Stage<float, NT> &st, f32x4_t (&acc)[NT], float &ss, bool live) {
+  float xv[8], gv[8], p[8];
+  Oct<float>::cvt(st.x, xv);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) xv[i] = live ? xv[i] : 0.f;
+  Oct<float>::cvt(st.g, gv);
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    ss = fmaf(xv[i], xv[i], ss);
+    p[i] = xv[i] * gv[i];
+  }
+#pragma unroll
+  for (int f = 0; f < NT; ++f) {
+    float wv[8];
+    Oct<float>::cvt(st.w[f], wv);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) acc[f] = __builtin_amdgcn_mfma_f32_16x16x4f32(p[i], wv[i], acc[f], 0, 0, 0);
   }
 }
 
-// NT = number of 16-expert tiles covered (N <= 16 * NT)
+// K blocks loaded together per wave: as many as fit in about 160 VGPRs, at most 4
+template <typename T, int NT> struct Depth {
+  static constexpr int regs = (2 + NT) * static_cast<int>(sizeof(typename Oct<T>::raw)) / 4;
+  static constexpr int fit = 160 / regs;
+  static constexpr int value = fit >= 4 ? 4 : fit >= 1 ? fit : 1;
+};
+
+// Blocks j = jfirst, jfirst + step, ... < jend of one wave: each round loads D
+// blocks, then multiplies them; indexes past jend are clamped (their data is
+// zeroed in the multiply), so every load is unconditional.
 template <typename T, int NT>
-__global__ __launch_bounds__(256) void route_kernel(RouteArgs a) {
+__device__ __forceinline__ void accumulate_logits(const T *xrow, const T *gl, const T *wl, const int (&woff)[NT],
+                                                  int jfirst, int jend, int step, f32x4_t (&acc)[NT], float &ss) {
+  constexpr int D = Depth<T, NT>::value;
+  const int last = jend - 1;
+  for (int j = jfirst; j < jend; j += D * step) {
+    Stage<T, NT> st[D];
+#pragma unroll
+    for (int u = 0; u < D; ++u) load_stage<T, NT>(st[u], xrow, gl, wl, woff, 32 * min(j + u * step, last));
+#pragma unroll
+    for (int u = 0; u < D; ++u) mma_stage<NT>(st[u], acc, ss, j + u * step < jend);
+  }
+}
+
+// One wave's partial logits of blocks jfirst, jfirst + step, ... < jend for
+// the 16 tokens from t0, into zred[token][expert] and ssred[token] (LDS).
+template <typename T, int NT, int ZS>
+__device__ __forceinline__ void wave_logits(const RouteArgs &a, int t0, int jfirst, int jend, int step,
+                                            float (*zred)[ZS], float *ssred) {
+  const T *x = static_cast<const T *>(a.x);
+  const int lane = threadIdx.x & 63;
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int d = a.d, N = a.N;
+  const int trow = min(t0 + r16, a.T - 1);  // rows past the batch repeat the last token
+  const T *xrow = x + static_cast<size_t>(trow) * d + grp * 8;
+  const T *gl = static_cast<const T *>(a.gamma) + grp * 8;
+  const T *wl = static_cast<const T *>(a.w_router) + grp * 8;
+  int woff[NT];
+#pragma unroll
+  for (int f = 0; f < NT; ++f) woff[f] = min(16 * f + r16, N - 1) * d;
+  f32x4_t acc[NT];
+#pragma unroll
+  for (int f = 0; f < NT; ++f) acc[f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  float ss = 0.f;
+  accumulate_logits<T, NT>(xrow, gl, wl, woff, jfirst, jend, step, acc, ss);
+  // D[row = token 4 grp + i][col = expert 16 f + r16]
+#pragma unroll
+  for (int f = 0; f < NT; ++f)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) zred[grp * 4 + i][16 * f + r16] = acc[f][i];
+  // lanes of token r16 are r16 + 16 g
+  ss += __shfl_xor(ss, 16);
+  ss += __shfl_xor(ss, 32);
+  if (grp == 0) ssred[r16] = ss;
+}
+
+constexpr int kPartWaves = 4;
+
+// Small batches: grid (chunks, K slices); workgroup (c, s) writes the partial
+// logits zpart[s][t][0..zstride) (before the RMS scale) and the partial sums
+// of squares sspart[s][t] of slice s for the tokens of chunk c.
+template <typename T, int NT>
+__global__ __launch_bounds__(256) void route_partial_kernel(RouteArgs a) {
+  constexpr int NP = NT * 16;
+  __shared__ float zred[kPartWaves][kTok][NP + 1];
+  __shared__ float ssred[kPartWaves][kTok];
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int t0 = blockIdx.x * kTok;
+  const int s = blockIdx.y;
+  const int nbs = (a.d >> 5) / a.ksplit;  // blocks per slice
+  wave_logits<T, NT, NP + 1>(a, t0, s * nbs + wave, (s + 1) * nbs, kPartWaves, zred[wave], ssred[wave]);
+  __syncthreads();
+  const size_t plane = static_cast<size_t>(s) * a.T;
+  for (int idx = tid; idx < kTok * NP; idx += 256) {
+    const int tl = idx / NP;
+    const int e = idx - tl * NP;
+    if (t0 + tl >= a.T) continue;
+    float z = 0.f;
+#pragma unroll
+    for (int w = 0; w < kPartWaves; ++w) z += zred[w][tl][e];
+    a.zpart[(plane + t0 + tl) * a.zstride + e] = z;
+  }
+  if (tid < kTok && t0 + tid < a.T) {
+    float ss = 0.f;
+#pragma unroll
+    for (int w = 0; w < kPartWaves; ++w) ss += ssred[w][tid];
+    a.sspart[plane + t0 + tid] = ss;
+  }
+}
+
+// NT = number of 16-expert tiles covered (N <= 16 * NT).  SPLIT: the logits
+// come from route_partial_kernel's K slices; otherwise the 8 waves compute
+// them here over all of K.
+template <typename T, int NT, bool SPLIT>
+__global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
+  constexpr int NP = NT * 16;
   const T *__restrict__ x = static_cast<const T *>(a.x);
   const T *__restrict__ gamma = static_cast<const T *>(a.gamma);
-  const T *__restrict__ wr = static_cast<const T *>(a.w_router);
   T *__restrict__ xn = static_cast<T *>(a.xn);
 
+  __shared__ float zred[SPLIT ? 1 : kWaves][kTok][NP + 1];  // per-wave partial logits; slot 0 ends as z
+  __shared__ float ssred[kWaves][kTok];
   __shared__ float rstd_s[kTok];
-  __shared__ float zp[4][kTok][NT * 16 + 1];
-  __shared__ uint32_t emask[NT * 16];
+  __shared__ uint32_t emask[NP];
+  __shared__ float a_gsp_s[NP], a_rcr_s[NP];
+  static_assert(512 % NP == 0, "a thread meets one expert column in the logits reduction");
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar loop control
   const int t0 = blockIdx.x * kTok;
-  const int d = a.d;
-  const int N = a.N;
-  for (int e = tid; e < NT * 16; e += 256) emask[e] = 0u;
-
-  // ---- 1. RMS scale per token
-  for (int j = 0; j < 4; ++j) {
-    const int tl = wave * 4 + j;
-    const int t = t0 + tl;
-    float ss = 0.f;
-    if (t < a.T) {
-      const T *row = x + static_cast<size_t>(t) * d;
-      for (int c = lane * 4; c < d; c += 256) {
-        float v[4];
-        load4<T>(row + c, v);
-        ss = fmaf(v[0], v[0], ss);
-        ss = fmaf(v[1], v[1], ss);
-        ss = fmaf(v[2], v[2], ss);
-        ss = fmaf(v[3], v[3], ss);
-      }
-    }
-    for (int off = 32; off > 0; off >>= 1) ss += __shfl_xor(ss, off);
-    if (lane == 0) rstd_s[tl] = (t < a.T) ? 1.0f / sqrtf(ss / static_cast<float>(d) + a.rms_eps) : 0.f;
+  const int d = a.d, N = a.N, nt = a.T;
+  if (tid < NP) {
+    emask[tid] = 0u;
+    a_gsp_s[tid] = tid < N ? a.a_gsp[tid] : 0.f;
+    a_rcr_s[tid] = tid < N ? a.a_rcr[tid] : 0.f;
   }
-  __syncthreads();
+  // router bias of this thread's expert column in the logits reduction below
+  const float bias = (a.b_router && (tid % NP) < N) ? a.b_router[tid % NP] : 0.f;
 
-  // ---- 2. router logits on fp32 MFMA, two accumulator sets (even / odd K blocks)
-  {
-    const int r16 = lane & 15;  // A row (token) / B column (expert within a tile)
-    const int grp = lane >> 4;  // K group of the MFMA operand
-    const int t = t0 + r16;
-    const bool tvalid = t < a.T;
-    const float rs = rstd_s[r16];
-    const int kq = d >> 2;         // this wave's K range, a multiple of 32
-    const int nb = kq >> 5;        // 32-wide K blocks
-    const int kbeg = wave * kq + grp * 8;
-    const T *xrow = x + static_cast<size_t>(tvalid ? t : 0) * d;
-    T *xnrow = xn + static_cast<size_t>(tvalid ? t : 0) * d;
-
-    f32x4_t acc0[NT], acc1[NT];
-#pragma unroll
-    for (int et = 0; et < NT; ++et) {
-      acc0[et] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-      acc1[et] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  if constexpr (SPLIT) {
+    // ---- 1. add the K slices' partial logits and sums of squares in slice order
+    if (tid < kTok) {
+      float ssum = 0.f;
+      for (int sl = 0; sl < a.ksplit; ++sl) ssum += a.sspart[static_cast<size_t>(sl) * nt + min(t0 + tid, nt - 1)];
+      rstd_s[tid] = 1.0f / sqrtf(ssum / static_cast<float>(d) + a.rms_eps);
     }
-    // the next block's operands are loaded before the current block's MFMAs
-    Block<T, NT> b0, b1;
-    load_block<T, NT>(b0, xrow, gamma, wr, d, N, r16, kbeg);
-    int j = 0;
-    for (; j + 1 < nb; j += 2) {
-      const int k = kbeg + 32 * j;
-      load_block<T, NT>(b1, xrow, gamma, wr, d, N, r16, k + 32);
-      mfma_block<T, NT>(b0, acc0, rs, tvalid, xnrow + k);
-      load_block<T, NT>(b0, xrow, gamma, wr, d, N, r16, kbeg + 32 * min(j + 2, nb - 1));
-      mfma_block<T, NT>(b1, acc1, rs, tvalid, xnrow + k + 32);
+    for (int idx = tid; idx < kTok * NP; idx += 512) {
+      const int tl = idx / NP;
+      const int e = idx - tl * NP;
+      const size_t col = static_cast<size_t>(min(t0 + tl, nt - 1)) * a.zstride + e;
+      float part[kRouteMaxSlices];
+#pragma unroll
+      for (int sl = 0; sl < kRouteMaxSlices; ++sl)
+        part[sl] = sl < a.ksplit ? a.zpart[static_cast<size_t>(sl) * nt * a.zstride + col] : 0.f;
+      float z = 0.f;
+#pragma unroll
+      for (int sl = 0; sl < kRouteMaxSlices; ++sl) z += part[sl];
+      zred[0][tl][e] = z;
     }
-    if (j < nb) mfma_block<T, NT>(b0, acc0, rs, tvalid, xnrow + kbeg + 32 * j);
-    // D[row = token 4*grp + i][col = expert et*16 + r16]
+    __syncthreads();
+    for (int idx = tid; idx < kTok * NP; idx += 512) {
+      const int tl = idx / NP;
+      const int e = idx - tl * NP;
+      zred[0][tl][e] = zred[0][tl][e] * rstd_s[tl] + bias;
+    }
+    __syncthreads();
+  } else {
+    // ---- 1. logits over all K: wave w takes blocks w, w + 8, ...
+    wave_logits<T, NT, NP + 1>(a, t0, wave, d >> 5, kWaves, zred[wave], ssred[wave]);
+    __syncthreads();
+    if (tid < kTok) {
+      float ssum = 0.f;
 #pragma unroll
-    for (int et = 0; et < NT; ++et)
+      for (int w = 0; w < kWaves; ++w) ssum += ssred[w][tid];
+      rstd_s[tid] = 1.0f / sqrtf(ssum / static_cast<float>(d) + a.rms_eps);
+    }
+    __syncthreads();
+    for (int idx = tid; idx < kTok * NP; idx += 512) {
+      const int tl = idx / NP;
+      const int e = idx - tl * NP;
+      float z = 0.f;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) zp[wave][grp * 4 + i][et * 16 + r16] = acc0[et][i] + acc1[et][i];
+      for (int w = 0; w < kWaves; ++w) z += zred[w][tl][e];
+      zred[0][tl][e] = z * rstd_s[tl] + bias;
+    }
+    __syncthreads();
   }
-  __syncthreads();
-  for (int idx = tid; idx < kTok * N; idx += 256) {
-    const int tl = idx / N;
-    const int e = idx - tl * N;
-    float z = (zp[0][tl][e] + zp[1][tl][e]) + (zp[2][tl][e] + zp[3][tl][e]);
-    if (a.b_router) z += a.b_router[e];
-    zp[0][tl][e] = z;
-  }
-  __syncthreads();
 
-  // ---- 3. top-k, gates and Alg. 4: one token per 16-lane group
-  const int k = a.k;
+  int my_e = -1;  // expert of this lane's slot (lane sub < k), -1 if none
+  bool my_kept = false;
   const int sub = lane & 15;
   const int tl = wave * 4 + (lane >> 4);
   const int t = t0 + tl;
-  const bool tvalid = t < a.T;
-  int my_e = -1;        // expert of this lane's slot (lane sub < k), -1 if none
-  bool my_kept = false;
-  {
-    const float *zrow = zp[0][tl];
-    float v[NT];
+  if (wave >= 4) {
+    // ---- x_in = x * rstd * gamma for the expert GEMMs (waves 4-7)
+    const int d8 = d >> 3;
+    for (int c8 = tid - 256; c8 < d8; c8 += 256) {
+      // all 16 rows in flight at once (rows past the batch load the last token, unused)
+      typename Oct<T>::raw xr[kTok];
+#pragma unroll
+      for (int u = 0; u < kTok; ++u) xr[u] = Oct<T>::load(x + static_cast<size_t>(min(t0 + u, nt - 1)) * d + 8 * c8);
+      float gv[8];
+      Oct<T>::cvt(Oct<T>::load(gamma + 8 * c8), gv);
+#pragma unroll
+      for (int u = 0; u < kTok; ++u) {
+        if (t0 + u >= nt) break;
+        float xv[8], av[8];
+        Oct<T>::cvt(xr[u], xv);
+        const float rs = rstd_s[u];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) av[i] = (xv[i] * rs) * gv[i];
+        Oct<T>::store(xn + static_cast<size_t>(t0 + u) * d + 8 * c8, av);
+      }
+    }
+  } else {
+    // ---- 2. top-k, gates and Alg. 4 (waves 0-3): one token per 16-lane
+    // group, lane `sub` holds slot `sub` (sub < k)
+    const int k = a.k;
+    const bool tvalid = t < nt;
+    const float *zrow = zred[0][tl];
+    // this lane's candidates, experts sub + 16 q, sorted; it can lose at most k <= 8 of them
+    uint64_t cand[NT];
 #pragma unroll
     for (int q = 0; q < NT; ++q) {
       const int e = sub + 16 * q;
-      v[q] = (e < N) ? zrow[e] : -INFINITY;
+      cand[q] = (e < N) ? topk_key(zrow[e], e) : 0ull;
     }
-    unsigned taken = 0;
-    int sel_e[kMaxK];
-    float sel_z[kMaxK];
+    sort_desc<NT>(cand);
+    constexpr int L = NT < kMaxK ? NT : kMaxK;
+    uint64_t head[L];
 #pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      sel_e[i] = 0;
-      sel_z[i] = 0.f;
-      if (i < k) {
-        float bv = -INFINITY;
-        int be = 0x7fffffff;
+    for (int q = 0; q < L; ++q) head[q] = cand[q];
+    // k rounds: the row maximum of the lanes' heads is the next slot; the lane
+    // that held it pops its head
+    uint64_t mykey = 0, topkey = 0;
+#pragma unroll 1
+    for (int i = 0; i < k; ++i) {
+      const uint64_t m = row_max64(head[0]);
+      if (i == 0) topkey = m;
+      if (sub == i) mykey = m;
+      const bool win = head[0] == m;
 #pragma unroll
-        for (int q = 0; q < NT; ++q) {
-          const int e = sub + 16 * q;
-          if (e < N && !((taken >> q) & 1u) && better(v[q], e, bv, be)) {
-            bv = v[q];
-            be = e;
-          }
-        }
-#pragma unroll
-        for (int off = 8; off > 0; off >>= 1) {
-          const float ov = __shfl_xor(bv, off, 16);
-          const int oe = __shfl_xor(be, off, 16);
-          if (better(ov, oe, bv, be)) {
-            bv = ov;
-            be = oe;
-          }
-        }
-        sel_e[i] = be;
-        sel_z[i] = bv;
-        if ((be & 15) == sub) taken |= 1u << (be >> 4);
-      }
+      for (int q = 0; q + 1 < L; ++q) head[q] = win ? head[q + 1] : head[q];
+      head[L - 1] = win ? 0ull : head[L - 1];
     }
-    // renormalised top-k gates
-    float gsel[kMaxK];
-    float gsum = 0.f;
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      gsel[i] = (i < k) ? expf(sel_z[i] - sel_z[0]) : 0.f;
-      gsum += gsel[i];
-    }
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) gsel[i] = gsel[i] / gsum;
-
+    const bool slot = sub < k;
+    const int se = slot ? key_expert(mykey) : 0;  // this lane's slot: expert and logit
+    const float sz = key_logit(mykey), ztop = key_logit(topkey);
+    // renormalised top-k gate
+    const float ge = slot ? expf(sz - ztop) : 0.f;
+    const float g = ge / group_sum(ge);
     // Alg. 4: s = g * A(e); p = s / (sum s + eps); c = max(p_GSP, p_RCR)
-    float sg[kMaxK], sr[kMaxK];
-    float zg = 0.f, zr = 0.f;
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      sg[i] = (i < k) ? gsel[i] * a.a_gsp[sel_e[i]] : 0.f;
-      sr[i] = (i < k) ? gsel[i] * a.a_rcr[sel_e[i]] : 0.f;
-      zg += sg[i];
-      zr += sr[i];
-    }
-    zg += a.eps;
-    zr += a.eps;
-    float c[kMaxK];
-    bool kept[kMaxK];
-    int nkept = 0;
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      const float pg = sg[i] / zg;
-      const float pr = sr[i] / zr;
-      c[i] = fmaxf(pg, pr);
-      // skip only if both views are below tau; slot 0 is the top-1 expert
-      const bool skip = !a.skip_disable && i > 0 && pg < a.tau && pr < a.tau;
-      kept[i] = (i < k) && !skip;
-      nkept += kept[i] ? 1 : 0;
-    }
+    const float sg = slot ? g * a_gsp_s[se] : 0.f;
+    const float sr = slot ? g * a_rcr_s[se] : 0.f;
+    const float pg = sg / (group_sum(sg) + a.eps);
+    const float pr = sr / (group_sum(sr) + a.eps);
+    const float c = fmaxf(pg, pr);
+    // skip only if both views are below tau; slot 0 is the top-1 expert
+    const bool skip = !a.skip_disable && sub > 0 && pg < a.tau && pr < a.tau;
+    bool kept = slot && !skip;
+    const int nkept = group_count(kept);
     if (!a.skip_disable && nkept < a.m_min) {
       // restore skipped slots by descending c (ties -> lower slot) up to m_min
-      const int need = a.m_min - nkept;
-      bool restore[kMaxK];
-#pragma unroll
-      for (int i = 0; i < kMaxK; ++i) {
-        int rank = 0;
-#pragma unroll
-        for (int jj = 0; jj < kMaxK; ++jj)
-          if (jj < k && !kept[jj] && jj != i && (c[jj] > c[i] || (c[jj] == c[i] && jj < i))) ++rank;
-        restore[i] = (i < k) && !kept[i] && rank < need;
+      int rank = 0;
+#pragma unroll 1
+      for (int jj = 0; jj < k; ++jj) {
+        const float cj = __shfl(c, jj, 16);
+        const int kj = __shfl(kept ? 1 : 0, jj, 16);
+        if (!kj && jj != sub && (cj > c || (cj == c && jj < sub))) ++rank;
       }
-#pragma unroll
-      for (int i = 0; i < kMaxK; ++i) kept[i] = kept[i] || restore[i];
+      kept = kept || (slot && rank < a.m_min - nkept);
     }
-    float zgate = 0.f;
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i)
-      if (kept[i]) zgate += gsel[i];
-    zgate += a.eps;
-
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      if (tvalid && i < k && i == sub) {
-        const size_t o = static_cast<size_t>(t) * k + i;
-        const float gh = a.skip_disable ? gsel[i] : (kept[i] ? gsel[i] / zgate : 0.f);
-        a.topk_idx[o] = sel_e[i];
-        a.keep[o] = kept[i] ? 1 : 0;
-        a.gates[o] = gh;
-        if (a.scores) a.scores[o] = c[i];
-        if (!kept[i]) a.slot_row[o] = -1;
-        my_e = sel_e[i];
-        my_kept = kept[i];
-      }
+    const float zgate = group_sum(kept ? g : 0.f) + a.eps;
+    if (tvalid && slot) {
+      const size_t o = static_cast<size_t>(t) * k + sub;
+      a.topk_idx[o] = se;
+      a.keep[o] = kept ? 1 : 0;
+      a.gates[o] = a.skip_disable ? g : (kept ? g / zgate : 0.f);
+      if (a.scores) a.scores[o] = c;
+      if (!kept) a.slot_row[o] = -1;
+      my_e = se;
+      my_kept = kept;
     }
   }
-  // ---- 4. per-expert token masks of this workgroup -> local ranks and counts
+  // ---- per-expert token masks of this chunk -> local ranks and counts
   if (my_kept) atomicOr(&emask[my_e], 1u << tl);
   __syncthreads();
   if (my_kept) {
     const uint32_t below = emask[my_e] & ((1u << tl) - 1u);
-    a.local_rank[static_cast<size_t>(t) * k + sub] = static_cast<uint8_t>(__popc(below));
+    a.local_rank[static_cast<size_t>(t) * a.k + sub] = static_cast<uint8_t>(__popc(below));
   }
-  for (int e = tid; e < N; e += 256)
+  for (int e = tid; e < N; e += 512)
     a.chunk_count[static_cast<size_t>(blockIdx.x) * N + e] = static_cast<uint8_t>(__popc(emask[e]));
+}
+
+template <typename T, int NT>
+void launch_route_nt(const RouteArgs &a, hipStream_t stream) {
+  const int chunks = (a.T + kTok - 1) / kTok;
+  if (a.ksplit > 0) {
+    route_partial_kernel<T, NT><<<dim3(chunks, a.ksplit), 256, 0, stream>>>(a);
+    route_kernel<T, NT, true><<<dim3(chunks), 512, 0, stream>>>(a);
+  } else {
+    route_kernel<T, NT, false><<<dim3(chunks), 512, 0, stream>>>(a);
+  }
 }
 
 template <typename T>
 hipError_t launch_route_t(const RouteArgs &a, hipStream_t stream) {
-  const dim3 grid((a.T + kTok - 1) / kTok);
-  const int nt = (a.N + 15) / 16;
-  if (nt <= 2)
-    route_kernel<T, 2><<<grid, 256, 0, stream>>>(a);
-  else if (nt <= 4)
-    route_kernel<T, 4><<<grid, 256, 0, stream>>>(a);
-  else if (nt <= 8)
-    route_kernel<T, 8><<<grid, 256, 0, stream>>>(a);
+  const int nt = route_expert_tiles(a.N);
+  if (nt == 1)
+    launch_route_nt<T, 1>(a, stream);
+  else if (nt == 2)
+    launch_route_nt<T, 2>(a, stream);
+  else if (nt == 4)
+    launch_route_nt<T, 4>(a, stream);
+  else if (nt == 8)
+    launch_route_nt<T, 8>(a, stream);
   else
-    route_kernel<T, 16><<<grid, 256, 0, stream>>>(a);
+    launch_route_nt<T, 16>(a, stream);
   return hipGetLastError();
 }
 
