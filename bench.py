@@ -59,6 +59,9 @@ def parse():
     ap.add_argument("--q", default="0.5", help="skip ratio whose stored tau is used")
     ap.add_argument("--prefill-only", action="store_true", help="time only the ACE prefill step")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="time only the decode batches (prints their JSON, not the prefill contract line)")
+    ap.add_argument("--decode-batches", default="1,8,32,64", help="comma-separated decode batch sizes")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle sample budget")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (calibrates HBM byte counters)")
@@ -205,6 +208,30 @@ def main():
         log(f"calibration copy of {args.calib_copy_mb} MiB done")
         del src, dst
 
+    def decode_legs():
+        """Decode batches through the same layer, tau transferred from prefill."""
+        dec = {}
+        for B in [int(b) for b in args.decode_batches.split(",") if b]:
+            xb = torch.from_numpy(synth.decode_inputs(cfg.with_(T=B), B, step=0)).to(dev).to(bf)
+            s_ace, o_ace = make_step(xb, False, tau)
+            s_top, _ = make_step(xb, True, tau)
+            ms_a = time_steps(s_ace, max(args.steps, 50), args.warmup, torch)
+            ms_t = time_steps(s_top, max(args.steps, 50), args.warmup, torch)
+            kb = o_ace["keep"].cpu().numpy()
+            ea = int((o_ace["counts"].cpu().numpy() > 0).sum())
+            bb, _ = layer_bytes(B, d, N, k, m, ea, int(kb.sum()))
+            dec[str(B)] = {"tokens_per_s": round(B / (ms_a * 1e-3), 1), "ms_per_step": round(ms_a, 4),
+                           "topk_ms_per_step": round(ms_t, 4), "speedup_vs_topk": round(ms_t / ms_a, 4),
+                           "realised_skip": round(1 - kb.mean(), 4), "experts_active": ea,
+                           "alg_gbs": round(bb / (ms_a * 1e-3) / 1e9, 1),
+                           "hbm_frac": round(bb / (ms_a * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            log(f"decode B={B}: {dec[str(B)]}")
+        return dec
+
+    if args.decode_only:
+        print(json.dumps({"decode": decode_legs()}), flush=True)
+        return
+
     # ---------------- prefill, ACE at the requested skip ratio
     ace_step, ace_out = make_step(D["x"], False, tau)
     log(f"timing prefill: {args.warmup} warmup + {args.steps} steps")
@@ -259,23 +286,7 @@ def main():
         log(f"plain top-k {ms_top:.3f} ms/step -> speedup {ms_top / ms:.3f}")
 
         # ---------------- decode batches, tau transferred from prefill
-        dec = {}
-        for B in (1, 8, 32, 64):
-            xb = torch.from_numpy(synth.decode_inputs(cfg.with_(T=B), B, step=0)).to(dev).to(bf)
-            s_ace, o_ace = make_step(xb, False, tau)
-            s_top, _ = make_step(xb, True, tau)
-            ms_a = time_steps(s_ace, max(args.steps, 50), args.warmup, torch)
-            ms_t = time_steps(s_top, max(args.steps, 50), args.warmup, torch)
-            kb = o_ace["keep"].cpu().numpy()
-            ea = int((o_ace["counts"].cpu().numpy() > 0).sum())
-            bb, _ = layer_bytes(B, d, N, k, m, ea, int(kb.sum()))
-            dec[str(B)] = {"tokens_per_s": round(B / (ms_a * 1e-3), 1), "ms_per_step": round(ms_a, 4),
-                           "topk_ms_per_step": round(ms_t, 4), "speedup_vs_topk": round(ms_t / ms_a, 4),
-                           "realised_skip": round(1 - kb.mean(), 4), "experts_active": ea,
-                           "alg_gbs": round(bb / (ms_a * 1e-3) / 1e9, 1),
-                           "hbm_frac": round(bb / (ms_a * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-            log(f"decode B={B}: {dec[str(B)]}")
-        result["decode"] = dec
+        result["decode"] = decode_legs()
 
     if not args.no_cpu and not args.prefill_only:
         log("timing the CPU oracle on a token sample")
