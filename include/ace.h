@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define ACE_ABI_VERSION 1
+#define ACE_ABI_VERSION 2
 
 typedef enum {
   ACE_OK = 0,
@@ -48,10 +48,27 @@ enum {
   /* Plain top-k layer through the same kernels: every routed slot is kept and
      ghat = g exactly (no epsilon).  This is the unskipped baseline. */
   ACE_SKIP_DISABLE = 1u << 0,
-  /* Fill outputs.scores with the ACE contribution c = max(p_GSP, p_RCR)
-     (Eq. ace_contribution) of every routed slot, as the App. C.1 score pass needs. */
+  /* Fill outputs.scores with the contribution c of every routed slot (under the
+     selected fusion rule; ACE: c = max(p_GSP, p_RCR), Eq. ace_contribution), as the
+     App. C.1 score pass needs. */
   ACE_WRITE_SCORES = 1u << 1
 };
+
+/* Contribution rule, stored in flags bits 2-4 as (rule << ACE_FUSION_SHIFT).  A slot
+   other than the top-1 is skippable iff c < tau; the m_min safeguard restores skipped
+   slots by descending c.  ACE is the max rule (Alg. 4); the others are the variants
+   the paper ablates (Tab. fusion_ablation, Tab. ablation) and its router-score
+   baseline (Sec. 4.1).  p_GSP, p_RCR are Eqs. gsp_probability, rcr_probability. */
+typedef enum {
+  ACE_FUSION_MAX = 0,   /* c = max(p_GSP, p_RCR): skip only if both views are low      */
+  ACE_FUSION_MIN = 1,   /* c = min(p_GSP, p_RCR): skip if either view is low (union)    */
+  ACE_FUSION_MEAN = 2,  /* c = (p_GSP + p_RCR) / 2                                      */
+  ACE_FUSION_GSP = 3,   /* c = p_GSP (single view)                                      */
+  ACE_FUSION_RCR = 4,   /* c = p_RCR (single view)                                      */
+  ACE_FUSION_SCORE = 5  /* c = g / (sum_j g_j + eps): router-score skipping, tables unused */
+} ace_fusion;
+#define ACE_FUSION_SHIFT 2
+#define ACE_FUSION_MASK (7u << ACE_FUSION_SHIFT)
 
 /* Layer shape and the scalars of Alg. 4. */
 typedef struct {
@@ -67,7 +84,7 @@ typedef struct {
   float tau;        /* threshold tau_q; a slot is skippable iff c < tau (strict) */
   float eps;        /* epsilon of Alg. 4 (both score normalisations and the gate renormalisation) */
   float rms_eps;    /* RMSNorm epsilon: x_in = x / sqrt(mean(x^2) + rms_eps) * gamma */
-  uint32_t flags;   /* ACE_SKIP_DISABLE | ACE_WRITE_SCORES */
+  uint32_t flags;   /* ACE_SKIP_DISABLE | ACE_WRITE_SCORES | (ace_fusion << ACE_FUSION_SHIFT) */
 } ace_moe_desc;
 
 /* Frozen layer parameters (DEVICE pointers, dtype = desc.dtype unless stated). */

@@ -68,8 +68,47 @@ def route(x_in, w_router, b_router, k: int):
     return z, pi, idx, g
 
 
-def ace_skip(g, a_gsp_e, a_rcr_e, tau: float, m_min: int, eps: float):
-    """Alg. 4 for one token.
+# Fusion rules of the per-slot contribution score (Sec. 4.3, Tab. fusion_ablation and
+# Tab. ablation; Sec. 4.1 baselines):
+#   "max"   c = max(p_GSP, p_RCR), the ACE rule (Eq. ace_contribution): skip only if
+#           both views are low, i.e. the intersection of the two candidate sets
+#           (Eq. ace_candidate_intersection)
+#   "min"   c = min(p_GSP, p_RCR): skip if either view is low (the union of the sets)
+#   "mean"  c = (p_GSP + p_RCR) / 2
+#   "gsp"   c = p_GSP (single view);  "rcr"  c = p_RCR (single view)
+#   "score" c = g / (sum g + eps): router-score skipping, the p of Alg. 4 with a
+#           table of ones
+FUSIONS = ("max", "min", "mean", "gsp", "rcr", "score")
+
+
+def contributions(g, a_gsp_e, a_rcr_e, eps: float, fusion: str = "max"):
+    """Per-slot (c, p_gsp, p_rcr) of one token under a fusion rule."""
+    g = f64(g)
+    # dual-view scores and their normalisation within the top-k set
+    # (Eqs. gsp_contribution, gsp_probability, rcr_contribution, rcr_probability)
+    s_gsp = g * f64(a_gsp_e)
+    s_rcr = g * f64(a_rcr_e)
+    p_gsp = s_gsp / (s_gsp.sum() + eps)
+    p_rcr = s_rcr / (s_rcr.sum() + eps)
+    if fusion == "max":
+        c = np.maximum(p_gsp, p_rcr)                  # Eq. ace_contribution
+    elif fusion == "min":
+        c = np.minimum(p_gsp, p_rcr)
+    elif fusion == "mean":
+        c = (p_gsp + p_rcr) / 2.0
+    elif fusion == "gsp":
+        c = p_gsp.copy()
+    elif fusion == "rcr":
+        c = p_rcr.copy()
+    elif fusion == "score":
+        c = g / (g.sum() + eps)
+    else:
+        raise ValueError(f"unknown fusion rule {fusion!r}")
+    return c, p_gsp, p_rcr
+
+
+def ace_skip(g, a_gsp_e, a_rcr_e, tau: float, m_min: int, eps: float, fusion: str = "max"):
+    """Alg. 4 for one token (with the fusion rule replaced for the ablation variants).
 
     g        [k] gates of the routed slots (slot order)
     a_gsp_e  [k] A^GSP(e_i) looked up for each slot
@@ -79,19 +118,16 @@ def ace_skip(g, a_gsp_e, a_rcr_e, tau: float, m_min: int, eps: float):
     """
     g = f64(g)
     k = g.shape[0]
-    # dual-view scores and their normalisation within the top-k set
-    # (Eqs. gsp_contribution, gsp_probability, rcr_contribution, rcr_probability)
-    s_gsp = g * f64(a_gsp_e)
-    s_rcr = g * f64(a_rcr_e)
-    z_gsp = s_gsp.sum() + eps
-    z_rcr = s_rcr.sum() + eps
-    p_gsp = s_gsp / z_gsp
-    p_rcr = s_rcr / z_rcr
-    c = np.maximum(p_gsp, p_rcr)                      # Eq. ace_contribution
-    # low-contribution candidate sets and their intersection (Eq. ace_candidate_intersection)
+    c, p_gsp, p_rcr = contributions(g, a_gsp_e, a_rcr_e, eps, fusion)
+    # low-contribution candidate sets of the two views
     s_gsp_set = {i for i in range(k) if p_gsp[i] < tau}
     s_rcr_set = {i for i in range(k) if p_rcr[i] < tau}
-    skip = s_gsp_set & s_rcr_set
+    if fusion == "max":
+        skip = s_gsp_set & s_rcr_set                  # Eq. ace_candidate_intersection
+    elif fusion == "min":
+        skip = s_gsp_set | s_rcr_set
+    else:
+        skip = {i for i in range(k) if c[i] < tau}
     # the top-1 routed expert is always retained
     top1 = max(range(k), key=lambda i: (g[i], -i))
     skip.discard(top1)
@@ -126,7 +162,7 @@ def expert_ffn(x_in_row, w_gate_e, w_up_e, w_down_e):
 
 def moe_forward(layer: dict, k: int, a_gsp, a_rcr, tau: float, m_min: int = 1,
                 eps: float = 1e-6, rms_eps: float = 1e-6, skip_disable: bool = False,
-                tokens=None, decisions=None):
+                tokens=None, decisions=None, fusion: str = "max"):
     """The online ACE layer forward (Alg. 1's online loop; Eq. ace_sparse_output).
 
     layer      dict with x, gamma, w_router, b_router, w_gate, w_up, w_down and
@@ -134,6 +170,7 @@ def moe_forward(layer: dict, k: int, a_gsp, a_rcr, tau: float, m_min: int = 1,
     k          top-k.
     a_gsp, a_rcr  [N] amplification tables (the values handed to the GPU).
     skip_disable  plain top-k layer: every slot kept and ghat = g exactly.
+    fusion     contribution rule (FUSIONS; "max" is ACE).
     tokens     optional iterable of token indices for which y is evaluated
                (routing and masks are always computed for every token).
     decisions  optional (topk_idx [T,k], keep [T,k]): evaluate y with these routing
@@ -159,7 +196,7 @@ def moe_forward(layer: dict, k: int, a_gsp, a_rcr, tau: float, m_min: int = 1,
     p_gsp = np.zeros((T, k))
     p_rcr = np.zeros((T, k))
     for t in range(T):
-        r = ace_skip(g[t], a_gsp[idx[t]], a_rcr[idx[t]], tau, m_min, eps)
+        r = ace_skip(g[t], a_gsp[idx[t]], a_rcr[idx[t]], tau, m_min, eps, fusion)
         c[t], p_gsp[t], p_rcr[t] = r["c"], r["p_gsp"], r["p_rcr"]
         if skip_disable:
             keep[t] = True

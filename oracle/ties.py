@@ -23,10 +23,9 @@ import numpy as np
 BAND = 1e-6
 
 
-def _alg4_scores(g, a_gsp_e, a_rcr_e, eps):
-    s_gsp = g * a_gsp_e
-    s_rcr = g * a_rcr_e
-    return np.maximum(s_gsp / (s_gsp.sum() + eps), s_rcr / (s_rcr.sum() + eps))
+def _alg4_scores(g, a_gsp_e, a_rcr_e, eps, fusion="max"):
+    from .forward import contributions
+    return contributions(g, a_gsp_e, a_rcr_e, eps, fusion)[0]
 
 
 def token_margins(z_row, idx_row, c_row, tau: float, m_min: int):
@@ -54,7 +53,7 @@ def is_tied(m: dict, band: float = BAND) -> bool:
 
 
 def admissible_token(z_row, pi_row, gpu_idx_row, gpu_keep_row, a_gsp, a_rcr, tau: float,
-                     m_min: int, eps: float, band: float = BAND):
+                     m_min: int, eps: float, band: float = BAND, fusion: str = "max"):
     """Can some resolution of the token's near-ties yield the GPU's decisions?"""
     z_row = np.asarray(z_row, dtype=np.float64)
     idx = np.asarray(gpu_idx_row, dtype=np.int64)
@@ -73,7 +72,7 @@ def admissible_token(z_row, pi_row, gpu_idx_row, gpu_keep_row, a_gsp, a_rcr, tau
         return False, "top-1 slot skipped"
     top = np.asarray(pi_row, dtype=np.float64)[idx]
     g = top / top.sum()
-    c = _alg4_scores(g, np.asarray(a_gsp, np.float64)[idx], np.asarray(a_rcr, np.float64)[idx], eps)
+    c = _alg4_scores(g, np.asarray(a_gsp, np.float64)[idx], np.asarray(a_rcr, np.float64)[idx], eps, fusion)
     skip_final = {i for i in range(1, k) if not keep[i]}
     clear_skip = {i for i in range(1, k) if c[i] < tau - band}
     ambiguous = [i for i in range(1, k) if abs(c[i] - tau) < band]
@@ -92,7 +91,7 @@ def admissible_token(z_row, pi_row, gpu_idx_row, gpu_keep_row, a_gsp, a_rcr, tau
 
 
 def compare_decisions(z, pi, oracle_idx, oracle_keep, c, gpu_idx, gpu_keep, a_gsp, a_rcr,
-                      tau: float, m_min: int, eps: float, band: float = BAND):
+                      tau: float, m_min: int, eps: float, band: float = BAND, fusion: str = "max"):
     """Bit-exact comparison of routing and masks with tie accounting.
 
     Returns dict(n_tokens, tied [list of token ids], mismatch_untied [ids whose
@@ -109,7 +108,7 @@ def compare_decisions(z, pi, oracle_idx, oracle_keep, c, gpu_idx, gpu_keep, a_gs
             if not same:
                 diff_tied.append(t)
                 ok, _ = admissible_token(z[t], pi[t], gpu_idx[t], gpu_keep[t], a_gsp, a_rcr,
-                                         tau, m_min, eps, band)
+                                         tau, m_min, eps, band, fusion)
                 if not ok:
                     inadm.append(t)
         elif not same:

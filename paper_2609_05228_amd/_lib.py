@@ -22,6 +22,9 @@ ACE_F32 = 0
 ACE_BF16 = 1
 ACE_SKIP_DISABLE = 1 << 0
 ACE_WRITE_SCORES = 1 << 1
+ACE_FUSION_SHIFT = 2
+# contribution rules (ace_fusion): ACE's max rule and the ablation variants
+FUSIONS = {"max": 0, "min": 1, "mean": 2, "gsp": 3, "rcr": 4, "score": 5}
 
 
 class Desc(ctypes.Structure):

@@ -78,6 +78,7 @@ struct RouteArgs {
   int T, d, N, k, m_min;
   float tau, eps, rms_eps;
   int skip_disable;
+  int fusion;             // ace_fusion: contribution rule (ACE: max)
 };
 
 struct PlanArgs {

@@ -116,7 +116,9 @@ ace_status validate(const ace_moe_desc *d, const void *x, const ace_moe_weights 
   if (std::isnan(d->tau) || !std::isfinite(d->eps) || d->eps < 0.f || !std::isfinite(d->rms_eps) ||
       d->rms_eps < 0.f)
     return ACE_ERR_INVALID_ARG;
-  if (d->flags & ~static_cast<uint32_t>(ACE_SKIP_DISABLE | ACE_WRITE_SCORES)) return ACE_ERR_INVALID_ARG;
+  if (d->flags & ~static_cast<uint32_t>(ACE_SKIP_DISABLE | ACE_WRITE_SCORES | ACE_FUSION_MASK))
+    return ACE_ERR_INVALID_ARG;
+  if (((d->flags & ACE_FUSION_MASK) >> ACE_FUSION_SHIFT) > ACE_FUSION_SCORE) return ACE_ERR_INVALID_ARG;
   if (d->N > ace::kMaxN || d->k > ace::kMaxK || d->d % 128 != 0 || d->m % 64 != 0 || d->d > 16384)
     return ACE_ERR_UNSUPPORTED;
   if (d->n_shared == 1 && d->m_shared % 64 != 0) return ACE_ERR_UNSUPPORTED;
@@ -291,6 +293,7 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   ra.eps = d.eps;
   ra.rms_eps = d.rms_eps;
   ra.skip_disable = (d.flags & ACE_SKIP_DISABLE) ? 1 : 0;
+  ra.fusion = static_cast<int>((d.flags & ACE_FUSION_MASK) >> ACE_FUSION_SHIFT);
   if (ace::launch_route(ra, bf16, stream) != hipSuccess) return ACE_ERR_HIP;
   mark(prof, 1, stream);
 

@@ -458,14 +458,26 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
     // renormalised top-k gate
     const float ge = slot ? expf(sz - ztop) : 0.f;
     const float g = ge / group_sum(ge);
-    // Alg. 4: s = g * A(e); p = s / (sum s + eps); c = max(p_GSP, p_RCR)
+    // Alg. 4: s = g * A(e); p = s / (sum s + eps); ACE: c = max(p_GSP, p_RCR)
     const float sg = slot ? g * a_gsp_s[se] : 0.f;
     const float sr = slot ? g * a_rcr_s[se] : 0.f;
     const float pg = sg / (group_sum(sg) + a.eps);
     const float pr = sr / (group_sum(sr) + a.eps);
-    const float c = fmaxf(pg, pr);
-    // skip only if both views are below tau; slot 0 is the top-1 expert
-    const bool skip = !a.skip_disable && sub > 0 && pg < a.tau && pr < a.tau;
+    float c;
+    switch (a.fusion) {
+      case 1: c = fminf(pg, pr); break;           // either view low (union)
+      case 2: c = (pg + pr) * 0.5f; break;        // mean of the views
+      case 3: c = pg; break;                      // GSP only
+      case 4: c = pr; break;                      // RCR only
+      case 5: {                                   // router score: the p of a table of ones
+        const float gs = slot ? g : 0.f;
+        c = gs / (group_sum(gs) + a.eps);
+        break;
+      }
+      default: c = fmaxf(pg, pr);                 // ACE: both views low (intersection)
+    }
+    // slot 0 is the top-1 expert, never skipped
+    const bool skip = !a.skip_disable && sub > 0 && c < a.tau;
     bool kept = slot && !skip;
     const int nkept = group_count(kept);
     if (!a.skip_disable && nkept < a.m_min) {

@@ -32,8 +32,11 @@ def _check(t, name, shape, dtype, device):
 
 
 def make_desc(T, d, N, k, m, dtype, tau, m_min=1, eps=1e-6, rms_eps=1e-6, n_shared=0, m_shared=0,
-              skip_disable=False, write_scores=False) -> _lib.Desc:
+              skip_disable=False, write_scores=False, fusion="max") -> _lib.Desc:
+    if fusion not in _lib.FUSIONS:
+        raise ValueError(f"fusion must be one of {sorted(_lib.FUSIONS)}")
     flags = (_lib.ACE_SKIP_DISABLE if skip_disable else 0) | (_lib.ACE_WRITE_SCORES if write_scores else 0)
+    flags |= _lib.FUSIONS[fusion] << _lib.ACE_FUSION_SHIFT
     dt = _DT[dtype] if isinstance(dtype, torch.dtype) else int(dtype)
     return _lib.Desc(T, d, N, k, m, n_shared, m_shared, dt, m_min, float(tau), float(eps),
                      float(rms_eps), flags)
@@ -53,7 +56,7 @@ def workspace(desc: _lib.Desc, device) -> torch.Tensor:
 def moe_forward(x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: int = 1,
                 eps: float = 1e-6, rms_eps: float = 1e-6, skip_disable: bool = False,
                 write_scores: bool = False, want_plan: bool = False, out: dict | None = None,
-                ws: torch.Tensor | None = None) -> dict:
+                ws: torch.Tensor | None = None, fusion: str = "max") -> dict:
     """One ACE MoE layer forward on the GPU.
 
     x        [T, d] bf16 or fp32 device tensor (the layer input before RMSNorm)
@@ -61,6 +64,8 @@ def moe_forward(x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: in
              w_gate / w_up [N, m, d], w_down [N, d, m], and optionally
              ws_gate / ws_up [m_s, d], ws_down [d, m_s] (one shared expert)
     a_gsp, a_rcr  [N] fp32 amplification tables
+    fusion   contribution rule: "max" (ACE) or an ablation variant
+             ("min", "mean", "gsp", "rcr", "score")
     Returns dict(y, topk_idx, keep, gates[, scores][, counts, offsets, perm]).
     """
     dev = x.device
@@ -88,7 +93,7 @@ def moe_forward(x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: in
     _check(a_rcr, "a_rcr", (N,), torch.float32, dev)
 
     desc = make_desc(T, d, N, k, m, dtype, tau, m_min, eps, rms_eps, 1 if shared else 0, ms,
-                     skip_disable, write_scores)
+                     skip_disable, write_scores, fusion)
     if out is None:
         out = {}
     o = dict(out)

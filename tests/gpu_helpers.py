@@ -37,12 +37,13 @@ def run_gpu(D: dict, a_gsp, a_rcr, k: int, tau: float, x=None, **kw) -> dict:
     return res
 
 
-def check_decisions(orc: dict, gpu: dict, a_gsp, a_rcr, tau: float, m_min: int, eps: float = 1e-6):
+def check_decisions(orc: dict, gpu: dict, a_gsp, a_rcr, tau: float, m_min: int, eps: float = 1e-6,
+                    fusion: str = "max"):
     """Bit-exact routing and masks, except admissible decisions of tied tokens."""
     rep = oracle.ties.compare_decisions(orc["z"], orc["pi"], orc["topk_idx"], orc["keep"], orc["c"],
                                         gpu["topk_idx"], gpu["keep"].astype(bool),
                                         np.asarray(a_gsp, np.float64), np.asarray(a_rcr, np.float64),
-                                        tau, m_min, eps)
+                                        tau, m_min, eps, fusion=fusion)
     assert not rep["mismatch_untied"], f"untied tokens differ: {rep['mismatch_untied'][:10]}"
     assert not rep["inadmissible"], f"tied tokens with inadmissible GPU decisions: {rep['inadmissible']}"
     return rep
@@ -76,14 +77,14 @@ def check_y(y_gpu, y_ref, dtype: str, rows=None):
 
 
 def full_check(L: dict, D: dict, a_gsp, a_rcr, tau: float, m_min: int = 1, tokens=None,
-               skip_disable: bool = False, eps: float = 1e-6):
+               skip_disable: bool = False, eps: float = 1e-6, fusion: str = "max"):
     """Run GPU and oracle on the same inputs and check decisions, plan, gates and y."""
     cfg = L["cfg"]
     gpu = run_gpu(D, a_gsp, a_rcr, cfg.k, tau, m_min=m_min, skip_disable=skip_disable,
-                  write_scores=True, eps=eps)
+                  write_scores=True, eps=eps, fusion=fusion)
     orc = oracle.forward.moe_forward(L, cfg.k, a_gsp, a_rcr, float(np.float32(tau)), m_min=m_min, eps=eps,
-                                     skip_disable=skip_disable, tokens=[])
-    rep = check_decisions(orc, gpu, a_gsp, a_rcr, float(np.float32(tau)), m_min, eps)
+                                     skip_disable=skip_disable, tokens=[], fusion=fusion)
+    rep = check_decisions(orc, gpu, a_gsp, a_rcr, float(np.float32(tau)), m_min, eps, fusion)
     check_plan(gpu, cfg.N)
     same = [t for t in range(cfg.T) if t not in set(rep["differing_tied"])]
     # gates and scores where decisions agree

@@ -176,6 +176,68 @@ def check_alg4_brute_force():
         assert {i for i in range(k) if not r["keep"][i]} == best, (g, ag, ar, tau, m_min)
 
 
+def check_fusion_variants_against_the_max_rule():
+    """The ablation variants (Tab. fusion_ablation, Tab. ablation; Sec. 4.1 Score)
+    against the ACE rule and against each other: the single views and router-score
+    skipping are the max rule with equal / all-ones tables; {max, min} = {p_GSP,
+    p_RCR}, so c_min + c_max = p_GSP + p_RCR = 2 c_mean; min is the union rule."""
+    F = oracle.forward
+    eps = 1e-6
+    for g, ag, ar, tau in _random_tokens(300, 6, 11):
+        r = {f: F.ace_skip(g, ag, ar, tau, 1, eps, f) for f in F.FUSIONS}
+        same_gsp = F.ace_skip(g, ag, ag, tau, 1, eps, "max")
+        same_rcr = F.ace_skip(g, ar, ar, tau, 1, eps, "max")
+        ones = F.ace_skip(g, np.ones(6), np.ones(6), tau, 1, eps, "max")
+        assert np.array_equal(r["gsp"]["keep"], same_gsp["keep"]) and np.allclose(r["gsp"]["c"], same_gsp["c"], rtol=0, atol=0)
+        assert np.array_equal(r["rcr"]["keep"], same_rcr["keep"]) and np.allclose(r["rcr"]["c"], same_rcr["c"], rtol=0, atol=0)
+        assert np.array_equal(r["score"]["keep"], ones["keep"]) and np.allclose(r["score"]["c"], ones["c"], rtol=1e-15, atol=0)
+        cmax, cmin, cmean = r["max"]["c"], r["min"]["c"], r["mean"]["c"]
+        assert np.all(cmin <= cmean) and np.all(cmean <= cmax) and np.all(cmin <= cmax)
+        assert np.allclose(cmin + cmax, 2 * cmean, rtol=1e-15, atol=1e-17)
+        # with m_min = 1 the skip sets nest: max inside mean inside min
+        sk = {f: {i for i in range(6) if not r[f]["keep"][i]} for f in F.FUSIONS}
+        assert sk["max"] <= sk["mean"] <= sk["min"]
+        # min is the union of the two views' candidate sets (top-1 excluded)
+        assert sk["min"] == (r["max"]["s_gsp_set"] | r["max"]["s_rcr_set"]) - {0}
+        for f in F.FUSIONS:
+            assert r[f]["keep"][0]
+            kept = r[f]["keep"]
+            assert np.allclose(r[f]["ghat"][kept], g[kept] / (g[kept].sum() + eps), atol=1e-15)
+
+
+def check_fusion_brute_force():
+    """Every variant obeys the same declarative characterisation as the ACE rule
+    (largest skippable subset leaving m_min active, least total c), with the
+    skippable slots taken from the two views directly."""
+    F = oracle.forward
+    rng = _rng(13)
+    for _ in range(200):
+        k = int(rng.integers(2, 6))
+        g = np.sort(rng.dirichlet(np.ones(k)))[::-1]
+        ag, ar = rng.uniform(0.3, 2.0, k), rng.uniform(0.3, 2.0, k)
+        tau = float(rng.uniform(0.0, 0.7))
+        m_min = int(rng.integers(1, k + 1))
+        p_g = g * ag / ((g * ag).sum() + 1e-6)
+        p_r = g * ar / ((g * ar).sum() + 1e-6)
+        low = {"max": lambda i: p_g[i] < tau and p_r[i] < tau,
+               "min": lambda i: p_g[i] < tau or p_r[i] < tau,
+               "mean": lambda i: p_g[i] + p_r[i] < 2 * tau,
+               "gsp": lambda i: p_g[i] < tau,
+               "rcr": lambda i: p_r[i] < tau,
+               "score": lambda i: g[i] < tau * (g.sum() + 1e-6)}
+        for f in F.FUSIONS:
+            r = F.ace_skip(g, ag, ar, tau, m_min, 1e-6, f)
+            c = r["c"]
+            skippable = [i for i in range(1, k) if low[f](i)]
+            best = None
+            for n in range(len(skippable), -1, -1):
+                if k - n < m_min:
+                    continue
+                best = min((set(S) for S in combinations(skippable, n)), key=lambda S: sum(c[i] for i in S))
+                break
+            assert {i for i in range(k) if not r["keep"][i]} == best, (f, g, ag, ar, tau, m_min)
+
+
 # --------------------------------------------------------------------------- output
 def check_dense_brute_force_output():
     L = tiny_layer(T=20, d=12, N=5, k=3, m=7, seed=8)

@@ -92,10 +92,13 @@ def test_null_and_misaligned_pointers():
     assert _call(_desc(n_shared=1, m_shared=128)) == _lib.ACE_ERR_INVALID_ARG
     # scores requested without a scores buffer
     assert _call(_desc(write_scores=True)) == _lib.ACE_ERR_INVALID_ARG
-    # unknown flag bit
-    d2 = _desc()
-    d2.flags = 1 << 7
-    assert _call(d2) == _lib.ACE_ERR_INVALID_ARG
+    # unknown flag bit, and fusion rules past ACE_FUSION_SCORE
+    for flags in (1 << 7, 6 << _lib.ACE_FUSION_SHIFT, 7 << _lib.ACE_FUSION_SHIFT):
+        d2 = _desc()
+        d2.flags = flags
+        assert _call(d2) == _lib.ACE_ERR_INVALID_ARG
+    with pytest.raises(ValueError):
+        _desc(fusion="median")
 
 
 def test_workspace_checked_before_launch():

@@ -19,8 +19,9 @@ import make_tables  # noqa: E402
 pytestmark = pytest.mark.gpu
 
 
-def _taus(L, a_gsp, a_rcr, qs, m_min=1):
-    base = oracle.forward.moe_forward(L, L["cfg"].k, a_gsp, a_rcr, tau=0.0, m_min=m_min, tokens=[])
+def _taus(L, a_gsp, a_rcr, qs, m_min=1, fusion="max"):
+    base = oracle.forward.moe_forward(L, L["cfg"].k, a_gsp, a_rcr, tau=0.0, m_min=m_min, tokens=[],
+                                      fusion=fusion)
     return {q: float(np.float32(t)) for q, t in oracle.tau.tau_table([base["c"]], m_min, qs).items()}
 
 
@@ -91,6 +92,28 @@ def test_small_f32_ragged():
     tau = _taus(L, tb["a_gsp"], tb["a_rcr"], [0.4])[0.4]
     r = full_check(L, device_layer(L), tb["a_gsp"], tb["a_rcr"], tau)
     _report("small f32 ragged", r)
+
+
+# ------------------------------------------------------------------ fusion and single-view variants
+@pytest.mark.parametrize("fusion", ["min", "mean", "gsp", "rcr", "score"])
+def test_fusion_variants_bf16(fusion):
+    """The ablation rules (Tab. fusion_ablation, Tab. ablation) and router-score
+    skipping, each at the threshold of its own 40% budget, with m_min = 2 so the
+    restore order by that rule's c is exercised too."""
+    L = synth.make_layer(synth.config("prefill_4096", T=300, d=256, N=32, k=6, m=128, seed=21))
+    tb = oracle.tables.build_tables(L)
+    tau = _taus(L, tb["a_gsp"], tb["a_rcr"], [0.4], m_min=2, fusion=fusion)[0.4]
+    r = full_check(L, device_layer(L), tb["a_gsp"], tb["a_rcr"], tau, m_min=2, fusion=fusion)
+    _report(f"fusion {fusion} tau={tau}", r)
+    assert abs((1 - r["gpu"]["keep"].mean()) - 0.4) < 0.02
+
+
+@pytest.mark.parametrize("fusion", ["min", "mean", "score"])
+def test_fusion_variants_f32(tiny, fusion):
+    L, D, ag, ar = tiny
+    tau = _taus(L, ag, ar, [0.25], fusion=fusion)[0.25]
+    r = full_check(L, D, ag, ar, tau, fusion=fusion)
+    _report(f"tiny_f32 fusion {fusion} tau={tau}", r)
 
 
 def test_empty_tokens():

@@ -40,7 +40,7 @@ def _route_no_renorm(x_in, w_router, b_router, k):
 def _skip_variant(kind):
     orig = F.ace_skip
 
-    def fn(g, a_gsp_e, a_rcr_e, tau, m_min, eps):
+    def fn(g, a_gsp_e, a_rcr_e, tau, m_min, eps, fusion="max"):
         g = np.asarray(g, float)
         k = len(g)
         s_g, s_r = g * a_gsp_e, g * a_rcr_e
@@ -68,6 +68,23 @@ def _skip_variant(kind):
         return dict(keep=np.array([i in active for i in range(k)]), ghat=ghat, c=c, p_gsp=p_g,
                     p_rcr=p_r, s_gsp_set=sg, s_rcr_set=sr, skip_set=skip)
     fn.orig = orig
+    return fn
+
+
+def _contrib_variant(kind):
+    orig = F.contributions
+
+    def fn(g, a_gsp_e, a_rcr_e, eps, fusion="max"):
+        c, p_g, p_r = orig(g, a_gsp_e, a_rcr_e, eps, fusion)
+        if kind == "min_is_max" and fusion == "min":
+            c = np.maximum(p_g, p_r)
+        elif kind == "mean_no_half" and fusion == "mean":
+            c = p_g + p_r
+        elif kind == "score_is_gsp" and fusion == "score":
+            c = p_g
+        elif kind == "rcr_is_gsp" and fusion == "rcr":
+            c = p_g
+        return c, p_g, p_r
     return fn
 
 
@@ -155,6 +172,10 @@ MUTANTS = {
     "skip_restore_ascending": [(F, "ace_skip", _skip_variant("restore_ascending"))],
     "skip_no_eps_final": [(F, "ace_skip", _skip_variant("no_eps_final"))],
     "skip_no_eps_in_p": [(F, "ace_skip", _skip_variant("no_eps_in_p"))],
+    "fusion_min_is_max": [(F, "contributions", _contrib_variant("min_is_max"))],
+    "fusion_mean_no_half": [(F, "contributions", _contrib_variant("mean_no_half"))],
+    "fusion_score_is_gsp": [(F, "contributions", _contrib_variant("score_is_gsp"))],
+    "fusion_rcr_is_gsp": [(F, "contributions", _contrib_variant("rcr_is_gsp"))],
     "ffn_silu_on_up": [(F, "expert_ffn", _ffn_silu_on_up), (TB, "expert_ffn", _ffn_silu_on_up)],
     "ffn_relu": [(F, "expert_ffn", _ffn_relu), (TB, "expert_ffn", _ffn_relu)],
     "gsp_up_path_only": [(TB, "gsp_raw", _gsp_up_only)],
