@@ -32,6 +32,7 @@ HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 METRIC = "MoE-layer tokens/s at 50% skip (prefill, decode); speedup vs plain top-k"
 TABLES = os.path.join(ROOT, "tests", "golden", "tables_prefill_4096_seed0.json")
+ZIPF_TABLES = os.path.join(ROOT, "tests", "golden", "tables_zipf_256_seed0.json")
 TRAFFIC = os.path.join(ROOT, "profiles", "prefill_4096_traffic.json")
 # stage -> (kernel name in the rocprofv3 traffic record, source file)
 STAGE_KERNEL = {"gateup": ("grouped_gemm_bf16_kernel<true, 8>", "expert_gemm.hip"),
@@ -62,6 +63,8 @@ def parse():
     ap.add_argument("--decode-only", action="store_true",
                     help="time only the decode batches (prints their JSON, not the prefill contract line)")
     ap.add_argument("--decode-batches", default="1,8,32,64", help="comma-separated decode batch sizes")
+    ap.add_argument("--zipf-only", action="store_true",
+                    help="time only the 256-expert Zipf workload (prints its JSON, not the contract line)")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle sample budget")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (calibrates HBM byte counters)")
@@ -183,20 +186,72 @@ def main():
     ag = torch.tensor(gold["a_gsp"], dtype=torch.float32, device=dev)
     ar = torch.tensor(gold["a_rcr"], dtype=torch.float32, device=dev)
 
-    def make_step(x, skip_disable, tau_):
-        desc = ace.make_desc(x.shape[0], d, N, k, m, bf, tau_, skip_disable=skip_disable)
+    def make_step(x, skip_disable, tau_, W=None, tables=None, k_=None):
+        """One layer call with preallocated outputs and workspace (the timed unit)."""
+        W = D if W is None else W
+        a_g, a_r = (ag, ar) if tables is None else tables
+        kk = k if k_ is None else k_
+        NN, mm, dd = W["w_gate"].shape
+        shared = W.get("ws_gate") is not None
+        desc = ace.make_desc(x.shape[0], dd, NN, kk, mm, bf, tau_, skip_disable=skip_disable,
+                             n_shared=1 if shared else 0, m_shared=W["ws_gate"].shape[0] if shared else 0)
         ws = torch.empty(ace.workspace_size(desc), dtype=torch.uint8, device=dev)
-        out = {"y": torch.empty_like(x), "topk_idx": torch.empty((x.shape[0], k), dtype=torch.int32, device=dev),
-               "keep": torch.empty((x.shape[0], k), dtype=torch.uint8, device=dev),
-               "gates": torch.empty((x.shape[0], k), dtype=torch.float32, device=dev),
-               "counts": torch.empty((N,), dtype=torch.int32, device=dev),
-               "offsets": torch.empty((N + 1,), dtype=torch.int32, device=dev),
-               "perm": torch.empty((x.shape[0] * k,), dtype=torch.int32, device=dev)}
+        out = {"y": torch.empty_like(x), "topk_idx": torch.empty((x.shape[0], kk), dtype=torch.int32, device=dev),
+               "keep": torch.empty((x.shape[0], kk), dtype=torch.uint8, device=dev),
+               "gates": torch.empty((x.shape[0], kk), dtype=torch.float32, device=dev),
+               "counts": torch.empty((NN,), dtype=torch.int32, device=dev),
+               "offsets": torch.empty((NN + 1,), dtype=torch.int32, device=dev),
+               "perm": torch.empty((x.shape[0] * kk,), dtype=torch.int32, device=dev)}
 
         def fn():
-            return ace.moe_forward(x, D, ag, ar, k=k, tau=tau_, skip_disable=skip_disable, out=out, ws=ws,
+            return ace.moe_forward(x, W, a_g, a_r, k=kk, tau=tau_, skip_disable=skip_disable, out=out, ws=ws,
                                    want_plan=True)
         return fn, out
+
+    def zipf_leg():
+        """The wider-pool layer: T=8192, 256 experts top-8 m=512, one shared expert
+        (m_s=512), Zipf-skewed router bias; its own 50% threshold."""
+        zcfg = synth.config("zipf_256")
+        zg = json.load(open(ZIPF_TABLES))
+        assert zg["config"]["T"] == zcfg.T and zg["config"]["N"] == zcfg.N and zg["config"]["seed"] == zcfg.seed
+        ZL = synth.make_layer(zcfg)
+        ZW = {key: torch.from_numpy(ZL[key]).to(dev).to(bf).contiguous()
+              for key in ("x", "gamma", "w_router", "w_gate", "w_up", "w_down", "ws_gate", "ws_up", "ws_down")}
+        ZW["b_router"] = torch.from_numpy(ZL["b_router"]).to(dev)
+        del ZL
+        zt = (torch.tensor(zg["a_gsp"], dtype=torch.float32, device=dev),
+              torch.tensor(zg["a_rcr"], dtype=torch.float32, device=dev))
+        ztau = float(zg["tau_f32"][args.q])
+        s_ace, o_ace = make_step(ZW["x"], False, ztau, ZW, zt, zcfg.k)
+        s_top, o_top = make_step(ZW["x"], True, ztau, ZW, zt, zcfg.k)
+        ms_a = time_steps(s_ace, args.steps, args.warmup, torch)
+        ms_t = time_steps(s_top, args.steps, args.warmup, torch)
+        st = stage_profile(s_ace, args.steps, ace, torch)
+        kb = o_ace["keep"].cpu().numpy()
+        cnt = o_ace["counts"].cpu().numpy()
+        n_kept, e_act = int(kb.sum()), int((cnt > 0).sum())
+        e_all = int((o_top["counts"].cpu().numpy() > 0).sum())
+        Tz, dz, mz, ms_ = zcfg.T, zcfg.d, zcfg.m, zcfg.m_shared
+        flops = 6 * dz * mz * n_kept + 6 * dz * ms_ * Tz
+        byts = 2 * 3 * dz * mz * e_act + 2 * zcfg.N * dz + 2 * 3 * dz * ms_ + 2 * 2 * Tz * dz + 13 * Tz * zcfg.k
+        t_lb = max(flops / (BF16_PEAK_TFLOPS * 1e12), byts / (HBM_PEAK_GBS * 1e9))
+        res = {"workload": "zipf_256: bf16 MoE layer, T=8192 d=2048 N=256 top-8 m=512, one shared expert "
+                           "(m_s=512), Zipf router bias s=1.1, ACE skip target 0.5 (seeded synthetic inputs)",
+               "tokens_per_s": round(Tz / (ms_a * 1e-3), 1), "ms_per_step": round(ms_a, 4),
+               "topk_ms_per_step": round(ms_t, 4), "speedup_vs_topk": round(ms_t / ms_a, 4), "tau": ztau,
+               "realised_skip": round(1 - kb.mean(), 5), "experts_active": e_act,
+               "experts_routed_topk": e_all, "largest_expert_rows": int(cnt.max()), "kept_slots": n_kept,
+               "stages_ms": {s_: round(v, 5) for s_, v in st.items()},
+               "layer_roofline": {"alg_bytes": int(byts), "mfma_flop": int(flops),
+                                  "bound": "hbm" if byts / (HBM_PEAK_GBS * 1e9) >= flops / (BF16_PEAK_TFLOPS * 1e12)
+                                  else "mfma", "t_lower_bound_ms": round(t_lb * 1e3, 4),
+                                  "frac": round(t_lb * 1e3 / ms_a, 4),
+                                  "mfma_tflops": round(flops / (ms_a * 1e-3) / 1e12, 1),
+                                  "hbm_gbs": round(byts / (ms_a * 1e-3) / 1e9, 1)}}
+        log(f"zipf_256: {res}")
+        del ZW, s_ace, s_top, o_ace, o_top
+        torch.cuda.empty_cache()
+        return res
 
     if args.calib_copy_mb:
         # a plain copy of known size, so per-dispatch FETCH_SIZE / WRITE_SIZE counters can be scaled
@@ -230,6 +285,9 @@ def main():
 
     if args.decode_only:
         print(json.dumps({"decode": decode_legs()}), flush=True)
+        return
+    if args.zipf_only:
+        print(json.dumps({"workloads": {"zipf_256": zipf_leg()}}), flush=True)
         return
 
     # ---------------- prefill, ACE at the requested skip ratio
@@ -287,6 +345,7 @@ def main():
 
         # ---------------- decode batches, tau transferred from prefill
         result["decode"] = decode_legs()
+        result["workloads"] = {"zipf_256": zipf_leg()}
 
     if not args.no_cpu and not args.prefill_only:
         log("timing the CPU oracle on a token sample")

@@ -175,3 +175,33 @@ def test_decode(prefill, B):
     Dd = dict(D, x=torch.from_numpy(xs).to(DEV).to(torch.bfloat16))
     r = full_check(Ld, Dd, ag, ar, gold["tau_f32"]["0.5"])
     _report(f"decode B={B}", r)
+
+
+# ------------------------------------------------------------------ full-size wider pool (256 experts, shared expert, Zipf router)
+@pytest.fixture(scope="module")
+def zipf():
+    cfg = synth.config("zipf_256")
+    gold = make_tables.load("zipf_256")
+    assert gold["config"]["T"] == cfg.T and gold["config"]["N"] == cfg.N and gold["config"]["seed"] == cfg.seed
+    L = synth.make_layer(cfg)
+    return L, device_layer(L), np.array(gold["a_gsp"], np.float32), np.array(gold["a_rcr"], np.float32), gold
+
+
+ZSAMPLE = list(range(0, 8192, 128)) + [8191]
+
+
+def test_zipf_256(zipf):
+    L, D, ag, ar, gold = zipf
+    tau = gold["tau_f32"]["0.5"]
+    r = full_check(L, D, ag, ar, tau, tokens=ZSAMPLE)
+    _report(f"zipf_256 q=0.5 tau={tau}", r)
+    assert abs((1 - r["gpu"]["keep"].mean()) - 0.5) < 1e-3
+    counts = r["gpu"]["counts"]
+    print(f"[zipf_256] experts active {(counts > 0).sum()} of {len(counts)}, largest {counts.max()} rows",
+          flush=True)
+
+
+def test_zipf_256_skip_disable(zipf):
+    L, D, ag, ar, gold = zipf
+    r = full_check(L, D, ag, ar, gold["tau_f32"]["0.5"], skip_disable=True, tokens=ZSAMPLE[::4])
+    assert r["gpu"]["keep"].all()
