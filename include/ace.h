@@ -159,6 +159,41 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
 ace_status ace_profile_begin(int max_calls);
 ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls);
 
+/*
+ * Budget-to-threshold mapping (App. C.1) on the device.  From the contribution
+ * scores of one unlabeled score pass (outputs.scores of ace_moe_forward with
+ * ACE_WRITE_SCORES; any tau, the scores do not depend on it), computes for each
+ * requested skip ratio q the threshold tau_q that realises it:
+ *   N_all  = n_rows * k routed slots;
+ *   N_cand = slots other than slot 0 (top-1) and, with m_min > 1, the m_min - 1
+ *            highest-c other slots of each row (ties to the lower slot);
+ *   m_q    = clip(round-half-even(q * N_all), 0, N_cand);
+ *   tau_q  = midpoint of the m_q-th and (m_q+1)-th smallest candidate scores when
+ *            they differ; on a tie at value v, v or the midpoint of v and the next
+ *            larger score, whichever realises a count closer to m_q (the lower count
+ *            on a draw); 0 when m_q = 0, +inf when m_q = N_cand.
+ * A pass over several layers is one call over their scores stacked as rows (one
+ * global tau per model).  With that tau, ace_moe_forward on the same inputs skips
+ * exactly the candidates with c < tau_q.  Midpoints are formed in fp64 from the
+ * fp32 scores and rounded once to fp32.
+ *   scores     DEVICE [n_rows, k] fp32 (row r = one token of one layer, slot 0 = top-1);
+ *              may be NULL when n_rows = 0.
+ *   q          HOST [n_q] skip ratios in [0, 1]; 1 <= n_q <= ACE_TAU_MAX_Q.
+ *   tau        DEVICE [n_q] fp32 out.
+ *   m_q        DEVICE [n_q] int64 out, optional (NULL): the target skip counts.
+ *   n_cand     DEVICE [1] int64 out, optional (NULL).
+ *   workspace  DEVICE scratch of ace_tau_workspace_size() bytes, 256-byte aligned.
+ * Enqueued on `stream` with no host synchronisation; deterministic.
+ * Errors: k outside 1..8, m_min outside 1..k, n_rows < 0, n_q outside
+ * 1..ACE_TAU_MAX_Q, q outside [0, 1] or NaN, NULL required pointers ->
+ * ACE_ERR_INVALID_ARG; small or misaligned workspace -> ACE_ERR_WORKSPACE.
+ */
+#define ACE_TAU_MAX_Q 8
+size_t ace_tau_workspace_size(void);
+ace_status ace_tau_map(const float *scores, int64_t n_rows, int32_t k, int32_t m_min, const double *q,
+                       int32_t n_q, float *tau, int64_t *m_q, int64_t *n_cand, void *workspace,
+                       size_t workspace_bytes, void *stream);
+
 /* Static, human-readable text of a status code (never NULL). */
 const char *ace_status_string(int status);
 

@@ -79,6 +79,13 @@ def lib() -> ctypes.CDLL:
         L.ace_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int,
                                       ctypes.POINTER(ctypes.c_int)]
         L.ace_profile_end.restype = ctypes.c_int
+        L.ace_tau_workspace_size.argtypes = []
+        L.ace_tau_workspace_size.restype = ctypes.c_size_t
+        L.ace_tau_map.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                  ctypes.POINTER(ctypes.c_double), ctypes.c_int32, ctypes.c_void_p,
+                                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                  ctypes.c_void_p]
+        L.ace_tau_map.restype = ctypes.c_int
         _lib = L
     return _lib
 
@@ -120,3 +127,20 @@ def forward_raw(desc: Desc, x_ptr: int, weights: Weights, outputs: Outputs, ws_p
     return int(lib().ace_moe_forward(ctypes.byref(desc), ctypes.c_void_p(x_ptr), ctypes.byref(weights),
                                      ctypes.byref(outputs), ctypes.c_void_p(ws_ptr),
                                      ctypes.c_size_t(ws_bytes), ctypes.c_void_p(stream)))
+
+
+TAU_MAX_Q = 8
+
+
+def tau_workspace_size() -> int:
+    return int(lib().ace_tau_workspace_size())
+
+
+def tau_map_raw(scores_ptr: int, n_rows: int, k: int, m_min: int, qs, tau_ptr: int, m_q_ptr: int,
+                n_cand_ptr: int, ws_ptr: int, ws_bytes: int, stream: int) -> int:
+    """ace_tau_map on plain integers; returns the ace_status."""
+    qa = (ctypes.c_double * max(len(qs), 1))(*[float(v) for v in qs])
+    return int(lib().ace_tau_map(ctypes.c_void_p(scores_ptr), ctypes.c_int64(n_rows), ctypes.c_int32(k),
+                                 ctypes.c_int32(m_min), qa, ctypes.c_int32(len(qs)), ctypes.c_void_p(tau_ptr),
+                                 ctypes.c_void_p(m_q_ptr), ctypes.c_void_p(n_cand_ptr), ctypes.c_void_p(ws_ptr),
+                                 ctypes.c_size_t(ws_bytes), ctypes.c_void_p(stream)))

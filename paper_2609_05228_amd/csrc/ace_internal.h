@@ -146,4 +146,11 @@ hipError_t launch_combine(const CombineArgs &a, bool bf16, hipStream_t stream);
 // n_rows = device count of rows in routed mode) or down
 hipError_t launch_skinny(const SkinnyArgs &a, bool gateup, const int32_t *n_rows, hipStream_t stream);
 
+// App. C.1 threshold mapping: up to kTauMaxQ budgets per call; workspace of tau_workspace_bytes()
+constexpr int kTauMaxQ = 8;
+size_t tau_workspace_bytes();
+hipError_t launch_tau_map(const float *scores, long long n_rows, int k, int m_min, const double *q, int n_q,
+                          float *tau, long long *m_q_out, long long *n_cand_out, void *workspace,
+                          hipStream_t stream);
+
 }  // namespace ace

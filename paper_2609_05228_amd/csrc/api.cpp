@@ -222,6 +222,30 @@ size_t ace_moe_workspace_size(const ace_moe_desc *desc) {
 
 int ace_abi_version(void) { return ACE_ABI_VERSION; }
 
+size_t ace_tau_workspace_size(void) { return ace::tau_workspace_bytes(); }
+
+ace_status ace_tau_map(const float *scores, int64_t n_rows, int32_t k, int32_t m_min, const double *q,
+                       int32_t n_q, float *tau, int64_t *m_q, int64_t *n_cand, void *workspace,
+                       size_t workspace_bytes, void *stream) {
+  static_assert(ACE_TAU_MAX_Q == ace::kTauMaxQ, "tau budget count");
+  if (k < 1 || k > ace::kMaxK || m_min < 1 || m_min > k || n_rows < 0 || n_q < 1 || n_q > ACE_TAU_MAX_Q)
+    return ACE_ERR_INVALID_ARG;
+  if (!q || !tau || (n_rows > 0 && !scores)) return ACE_ERR_INVALID_ARG;
+  if (n_rows > (static_cast<int64_t>(1) << 40)) return ACE_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(scores) & 3) || (reinterpret_cast<uintptr_t>(tau) & 3) ||
+      (reinterpret_cast<uintptr_t>(m_q) & 7) || (reinterpret_cast<uintptr_t>(n_cand) & 7))
+    return ACE_ERR_INVALID_ARG;
+  for (int i = 0; i < n_q; ++i)
+    if (!(q[i] >= 0.0 && q[i] <= 1.0)) return ACE_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < ace::tau_workspace_bytes() ||
+      (reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)))
+    return ACE_ERR_WORKSPACE;
+  const hipError_t e = ace::launch_tau_map(scores, n_rows, k, m_min, q, n_q, tau, reinterpret_cast<long long *>(m_q),
+                                           reinterpret_cast<long long *>(n_cand), workspace,
+                                           static_cast<hipStream_t>(stream));
+  return e == hipSuccess ? ACE_OK : ACE_ERR_HIP;
+}
+
 const char *ace_status_string(int s) {
   switch (s) {
     case ACE_OK: return "ACE_OK: success";

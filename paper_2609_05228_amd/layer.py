@@ -121,3 +121,27 @@ def moe_forward(x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: in
     if st != _lib.ACE_OK:
         raise _lib.AceError(st, _lib.status_string(st))
     return o
+
+
+def tau_map(scores: torch.Tensor, qs, m_min: int = 1) -> dict:
+    """App. C.1 threshold mapping on the GPU.
+
+    scores  [R, k] fp32 device tensor: contribution scores c of a score pass
+            (one or more layers stacked as rows; slot 0 is each row's top-1)
+    qs      skip ratios in [0, 1] (at most 8)
+    Returns dict(tau [n_q] fp32, m_q [n_q] int64, n_cand [1] int64), device tensors,
+    enqueued on the current stream."""
+    if scores.dim() != 2 or scores.dtype != torch.float32 or not scores.is_contiguous():
+        raise ValueError("scores must be a contiguous [R, k] float32 tensor")
+    dev = scores.device
+    qs = [float(v) for v in qs]
+    tau = torch.empty(len(qs), dtype=torch.float32, device=dev)
+    m_q = torch.empty(len(qs), dtype=torch.int64, device=dev)
+    n_cand = torch.empty(1, dtype=torch.int64, device=dev)
+    ws = torch.empty(_lib.tau_workspace_size(), dtype=torch.uint8, device=dev)
+    st = _lib.tau_map_raw(scores.data_ptr() if scores.numel() else 0, scores.shape[0], scores.shape[1], m_min, qs,
+                          tau.data_ptr(), m_q.data_ptr(), n_cand.data_ptr(), ws.data_ptr(), ws.numel(),
+                          torch.cuda.current_stream(dev).cuda_stream)
+    if st != _lib.ACE_OK:
+        raise _lib.AceError(st, _lib.status_string(st))
+    return dict(tau=tau, m_q=m_q, n_cand=n_cand)

@@ -127,3 +127,20 @@ def test_product_path_never_touches_the_oracle():
             if f.endswith((".py", ".hip", ".cpp", ".h")):
                 text = open(os.path.join(dirpath, f)).read()
                 assert not re.search(r"\boracle\b", text), f"{f} mentions the oracle"
+
+
+def test_tau_map_validation():
+    need = ace.tau_workspace_size()
+    assert need > 0
+    ok = dict(scores=FAKE, n_rows=4, k=8, m_min=1, qs=[0.5], tau=FAKE, ws=FAKE, ws_bytes=need)
+
+    def call(**kw):
+        a = dict(ok, **kw)
+        return ace.tau_map_raw(a["scores"], a["n_rows"], a["k"], a["m_min"], a["qs"], a["tau"], 0, 0,
+                               a["ws"], a["ws_bytes"], 0)
+    for kw in (dict(k=0), dict(k=9), dict(m_min=0), dict(m_min=9, k=8), dict(n_rows=-1), dict(qs=[]),
+               dict(qs=[0.5] * 9), dict(qs=[1.01]), dict(qs=[-1e-9]), dict(qs=[float("nan")]),
+               dict(tau=0), dict(scores=0), dict(scores=FAKE + 2)):
+        assert call(**kw) == _lib.ACE_ERR_INVALID_ARG, kw
+    for kw in (dict(ws=0), dict(ws_bytes=need - 1), dict(ws=FAKE + 16)):
+        assert call(**kw) == _lib.ACE_ERR_WORKSPACE, kw
