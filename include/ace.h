@@ -188,6 +188,25 @@ ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls);
  * 1..ACE_TAU_MAX_Q, q outside [0, 1] or NaN, NULL required pointers ->
  * ACE_ERR_INVALID_ARG; small or misaligned workspace -> ACE_ERR_WORKSPACE.
  */
+/*
+ * Offline per-expert amplification tables on the device: A^GSP by Alg. 2 (Eqs.
+ * gsp_up_path, gsp_gate_path, gsp_geometric_mean, gsp_layer_normalization; the
+ * Frobenius norms of the two [d, d] products come from m x m Gram matrices on fp64
+ * MFMA) and A^RCR by Alg. 3 (Eqs. rcr_centered_router, rcr_direction_prototype with
+ * rho = 1, rcr_raw_amplification with the prototype as the expert input,
+ * rcr_layer_normalization).  fp64 throughout; deterministic.
+ *   desc       reads N, d, m, dtype and eps (the other fields are ignored).
+ *   w          reads gamma, w_router, w_gate, w_up, w_down (layouts as ace_moe_weights).
+ *   a_gsp, a_rcr      DEVICE [N] fp32 out: the tables ace_moe_forward takes.
+ *   a_gsp64, a_rcr64  DEVICE [N] fp64 out, optional (NULL).
+ *   workspace  DEVICE scratch of ace_tables_workspace_size(desc) bytes, 256-byte aligned.
+ * Requires m % 64 == 0 and d % 32 == 0 (else ACE_ERR_UNSUPPORTED).
+ */
+size_t ace_tables_workspace_size(const ace_moe_desc *desc);
+ace_status ace_build_tables(const ace_moe_desc *desc, const ace_moe_weights *w, float *a_gsp, float *a_rcr,
+                            double *a_gsp64, double *a_rcr64, void *workspace, size_t workspace_bytes,
+                            void *stream);
+
 #define ACE_TAU_MAX_Q 8
 size_t ace_tau_workspace_size(void);
 ace_status ace_tau_map(const float *scores, int64_t n_rows, int32_t k, int32_t m_min, const double *q,

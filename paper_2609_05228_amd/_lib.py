@@ -79,6 +79,12 @@ def lib() -> ctypes.CDLL:
         L.ace_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int,
                                       ctypes.POINTER(ctypes.c_int)]
         L.ace_profile_end.restype = ctypes.c_int
+        L.ace_tables_workspace_size.argtypes = [ctypes.POINTER(Desc)]
+        L.ace_tables_workspace_size.restype = ctypes.c_size_t
+        L.ace_build_tables.argtypes = [ctypes.POINTER(Desc), ctypes.POINTER(Weights), ctypes.c_void_p,
+                                       ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                       ctypes.c_size_t, ctypes.c_void_p]
+        L.ace_build_tables.restype = ctypes.c_int
         L.ace_tau_workspace_size.argtypes = []
         L.ace_tau_workspace_size.restype = ctypes.c_size_t
         L.ace_tau_map.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
@@ -144,3 +150,16 @@ def tau_map_raw(scores_ptr: int, n_rows: int, k: int, m_min: int, qs, tau_ptr: i
                                  ctypes.c_int32(m_min), qa, ctypes.c_int32(len(qs)), ctypes.c_void_p(tau_ptr),
                                  ctypes.c_void_p(m_q_ptr), ctypes.c_void_p(n_cand_ptr), ctypes.c_void_p(ws_ptr),
                                  ctypes.c_size_t(ws_bytes), ctypes.c_void_p(stream)))
+
+
+def tables_workspace_size(desc: Desc) -> int:
+    return int(lib().ace_tables_workspace_size(ctypes.byref(desc)))
+
+
+def build_tables_raw(desc: Desc, weights: Weights, gsp_ptr: int, rcr_ptr: int, gsp64_ptr: int, rcr64_ptr: int,
+                     ws_ptr: int, ws_bytes: int, stream: int) -> int:
+    """ace_build_tables on plain integers/structs; returns the ace_status."""
+    return int(lib().ace_build_tables(ctypes.byref(desc), ctypes.byref(weights), ctypes.c_void_p(gsp_ptr),
+                                      ctypes.c_void_p(rcr_ptr), ctypes.c_void_p(gsp64_ptr),
+                                      ctypes.c_void_p(rcr64_ptr), ctypes.c_void_p(ws_ptr), ctypes.c_size_t(ws_bytes),
+                                      ctypes.c_void_p(stream)))

@@ -146,6 +146,19 @@ hipError_t launch_combine(const CombineArgs &a, bool bf16, hipStream_t stream);
 // n_rows = device count of rows in routed mode) or down
 hipError_t launch_skinny(const SkinnyArgs &a, bool gateup, const int32_t *n_rows, hipStream_t stream);
 
+// Offline GSP / RCR tables (Alg. 2, Alg. 3) in fp64
+struct TablesCall {
+  const void *gamma, *w_router, *w_gate, *w_up, *w_down;
+  int N, d, m;
+  double eps;
+  bool bf16;
+  void *workspace;  // tables_workspace_bytes(N, d, m)
+  float *a_gsp, *a_rcr;
+  double *a_gsp64, *a_rcr64;  // optional
+};
+size_t tables_workspace_bytes(int N, int d, int m);
+hipError_t launch_tables(const TablesCall &c, hipStream_t stream);
+
 // App. C.1 threshold mapping: up to kTauMaxQ budgets per call; workspace of tau_workspace_bytes()
 constexpr int kTauMaxQ = 8;
 size_t tau_workspace_bytes();

@@ -222,6 +222,48 @@ size_t ace_moe_workspace_size(const ace_moe_desc *desc) {
 
 int ace_abi_version(void) { return ACE_ABI_VERSION; }
 
+size_t ace_tables_workspace_size(const ace_moe_desc *desc) {
+  if (!desc || desc->N <= 0 || desc->d <= 0 || desc->m <= 0) return 0;
+  return ace::tables_workspace_bytes(desc->N, desc->d, desc->m);
+}
+
+ace_status ace_build_tables(const ace_moe_desc *desc, const ace_moe_weights *w, float *a_gsp, float *a_rcr,
+                            double *a_gsp64, double *a_rcr64, void *workspace, size_t workspace_bytes,
+                            void *stream) {
+  if (!desc || !w || !a_gsp || !a_rcr) return ACE_ERR_INVALID_ARG;
+  const ace_moe_desc &d = *desc;
+  if (d.N <= 0 || d.d <= 0 || d.m <= 0 || (d.dtype != ACE_F32 && d.dtype != ACE_BF16) || !(d.eps >= 0.f))
+    return ACE_ERR_INVALID_ARG;
+  if (d.m % 64 != 0 || d.d % 32 != 0) return ACE_ERR_UNSUPPORTED;
+  const size_t align = 16;  // 16-byte operand loads
+  const void *need[] = {w->gamma, w->w_router, w->w_gate, w->w_up, w->w_down};
+  for (const void *p : need)
+    if (!p || (reinterpret_cast<uintptr_t>(p) & (align - 1))) return ACE_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(a_gsp) & 3) || (reinterpret_cast<uintptr_t>(a_rcr) & 3) ||
+      (reinterpret_cast<uintptr_t>(a_gsp64) & 7) || (reinterpret_cast<uintptr_t>(a_rcr64) & 7))
+    return ACE_ERR_INVALID_ARG;
+  if (!workspace || workspace_bytes < ace::tables_workspace_bytes(d.N, d.d, d.m) ||
+      (reinterpret_cast<uintptr_t>(workspace) & (kAlign - 1)))
+    return ACE_ERR_WORKSPACE;
+  ace::TablesCall c{};
+  c.gamma = w->gamma;
+  c.w_router = w->w_router;
+  c.w_gate = w->w_gate;
+  c.w_up = w->w_up;
+  c.w_down = w->w_down;
+  c.N = d.N;
+  c.d = d.d;
+  c.m = d.m;
+  c.eps = d.eps;
+  c.bf16 = d.dtype == ACE_BF16;
+  c.workspace = workspace;
+  c.a_gsp = a_gsp;
+  c.a_rcr = a_rcr;
+  c.a_gsp64 = a_gsp64;
+  c.a_rcr64 = a_rcr64;
+  return ace::launch_tables(c, static_cast<hipStream_t>(stream)) == hipSuccess ? ACE_OK : ACE_ERR_HIP;
+}
+
 size_t ace_tau_workspace_size(void) { return ace::tau_workspace_bytes(); }
 
 ace_status ace_tau_map(const float *scores, int64_t n_rows, int32_t k, int32_t m_min, const double *q,

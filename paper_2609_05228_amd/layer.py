@@ -145,3 +145,37 @@ def tau_map(scores: torch.Tensor, qs, m_min: int = 1) -> dict:
     if st != _lib.ACE_OK:
         raise _lib.AceError(st, _lib.status_string(st))
     return dict(tau=tau, m_q=m_q, n_cand=n_cand)
+
+
+def build_tables(weights: dict, eps: float = 1e-6, want_f64: bool = False) -> dict:
+    """GSP (Alg. 2) and RCR (Alg. 3) tables of one layer on the GPU, fp64 inside.
+
+    weights  dict: gamma [d], w_router [N, d], w_gate / w_up [N, m, d], w_down [N, d, m]
+             (bf16 or fp32 device tensors, one dtype)
+    Returns dict(a_gsp, a_rcr) as [N] fp32 device tensors (plus a_gsp64, a_rcr64 in
+    fp64 with want_f64), enqueued on the current stream."""
+    wg = weights["w_gate"]
+    N, m, d = wg.shape
+    dtype = wg.dtype
+    if dtype not in _DT:
+        raise ValueError(f"unsupported dtype {dtype}")
+    dev = wg.device
+    _check(weights["gamma"], "gamma", (d,), dtype, dev)
+    _check(weights["w_router"], "w_router", (N, d), dtype, dev)
+    _check(weights["w_up"], "w_up", (N, m, d), dtype, dev)
+    _check(weights["w_down"], "w_down", (N, d, m), dtype, dev)
+    desc = make_desc(1, d, N, 1, m, dtype, 0.0, eps=eps)
+    W = _lib.Weights(_ptr(weights["gamma"]), _ptr(weights["w_router"]), 0, _ptr(wg), _ptr(weights["w_up"]),
+                     _ptr(weights["w_down"]), 0, 0, 0, 0, 0)
+    out = {"a_gsp": torch.empty(N, dtype=torch.float32, device=dev),
+           "a_rcr": torch.empty(N, dtype=torch.float32, device=dev)}
+    if want_f64:
+        out["a_gsp64"] = torch.empty(N, dtype=torch.float64, device=dev)
+        out["a_rcr64"] = torch.empty(N, dtype=torch.float64, device=dev)
+    ws = torch.empty(max(_lib.tables_workspace_size(desc), 256), dtype=torch.uint8, device=dev)
+    st = _lib.build_tables_raw(desc, W, _ptr(out["a_gsp"]), _ptr(out["a_rcr"]), _ptr(out.get("a_gsp64")),
+                               _ptr(out.get("a_rcr64")), _ptr(ws), ws.numel(),
+                               torch.cuda.current_stream(dev).cuda_stream)
+    if st != _lib.ACE_OK:
+        raise _lib.AceError(st, _lib.status_string(st))
+    return out

@@ -5,7 +5,7 @@ It holds none of the method's arithmetic, so both the CPU oracle's tests and
 the GPU path's tests and benchmark can take their inputs from it without the
 two sides sharing any computation.
 """
-from .configs import CONFIGS, LayerConfig, config
+from .configs import CONFIGS, STACK_LAYERS, LayerConfig, config
 from .gen import (
     bf16_bits_to_f32,
     decode_inputs,
@@ -16,6 +16,7 @@ from .gen import (
 
 __all__ = [
     "CONFIGS",
+    "STACK_LAYERS",
     "LayerConfig",
     "config",
     "bf16_bits_to_f32",

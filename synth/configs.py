@@ -40,7 +40,11 @@ CONFIGS = {
     # wider pool with one shared expert and Zipf-skewed expert popularity
     "zipf_256": LayerConfig("zipf_256", T=8192, d=2048, N=256, k=8, m=512,
                             n_shared=1, m_shared=512, zipf_s=1.1),
+    # one layer of the 48-layer stack (layer l is make_layer(cfg, layer=l)); 8192-token prefill
+    "stack_48": LayerConfig("stack_48", T=8192, d=2048, N=128, k=8, m=768),
 }
+
+STACK_LAYERS = 48
 
 
 def config(name: str, **overrides) -> LayerConfig:

@@ -1,6 +1,7 @@
 """Write the offline GSP/RCR tables and the App. C.1 thresholds of a workload.
 
     python tests/golden/make_tables.py prefill_4096 [zipf_256 ...]
+    python tests/golden/make_tables.py stack_48      (tables of every layer; no tau)
 
 Calls only the seeded generators (synth) and the CPU oracle: GSP by Alg. 2,
 RCR by Alg. 3 (fp64, rounded once to fp32), and tau_q by the App. C.1 mapping
@@ -59,6 +60,27 @@ def make(name: str, seed: int = 0) -> dict:
     return out
 
 
+def make_stack(name: str = "stack_48", seed: int = 0) -> dict:
+    """GSP/RCR tables of every layer of the stack (the threshold of a stack comes
+    from its own score pass through the residual chain, so none is stored)."""
+    cfg = synth.config(name, seed=seed)
+    t0 = time.time()
+    layers = []
+    for li in range(synth.STACK_LAYERS):
+        L = synth.make_layer(cfg.with_(T=16), layer=li)   # weights only matter here
+        tb = oracle.tables.build_tables(L)
+        layers.append({"a_gsp": [float(v) for v in tb["a_gsp"]], "a_rcr": [float(v) for v in tb["a_rcr"]]})
+        print(f"layer {li} done at {time.time() - t0:.0f}s", flush=True)
+    out = {"config": dataclasses.asdict(cfg), "layers_count": synth.STACK_LAYERS,
+           "source": "oracle: Alg. 2 (GSP) and Alg. 3 (RCR) per layer in fp64 rounded to fp32; "
+                     "layer l's weights are synth.make_layer(config, layer=l)",
+           "command": f"python tests/golden/make_tables.py {name}", "eps": 1e-6, "layers": layers,
+           "seconds": round(time.time() - t0, 1)}
+    with open(table_path(name, seed), "w") as f:
+        json.dump(out, f)
+    return out
+
+
 def load(name: str, seed: int = 0) -> dict:
     with open(table_path(name, seed)) as f:
         return json.load(f)
@@ -66,5 +88,9 @@ def load(name: str, seed: int = 0) -> dict:
 
 if __name__ == "__main__":
     for n in sys.argv[1:] or ["prefill_4096"]:
+        if n.startswith("stack"):
+            r = make_stack(n)
+            print(n, r["seconds"])
+            continue
         r = make(n)
         print(n, r["tau"], r["seconds"])

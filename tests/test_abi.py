@@ -144,3 +144,21 @@ def test_tau_map_validation():
         assert call(**kw) == _lib.ACE_ERR_INVALID_ARG, kw
     for kw in (dict(ws=0), dict(ws_bytes=need - 1), dict(ws=FAKE + 16)):
         assert call(**kw) == _lib.ACE_ERR_WORKSPACE, kw
+
+
+def test_build_tables_validation():
+    d = _desc(d=256, N=8, m=512)
+    need = ace.tables_workspace_size(d)
+    assert need > 0
+
+    def call(desc=d, w=None, gsp=FAKE, rcr=FAKE, ws=FAKE, ws_bytes=need):
+        if w is None:
+            w = _lib.Weights(FAKE, FAKE, 0, FAKE, FAKE, FAKE, 0, 0, 0, 0, 0)
+        return ace.build_tables_raw(desc, w, gsp, rcr, 0, 0, ws, ws_bytes, 0)
+    assert call(desc=_desc(m=96)) == _lib.ACE_ERR_UNSUPPORTED       # m % 64
+    assert call(desc=_desc(d=200, m=512)) == _lib.ACE_ERR_UNSUPPORTED
+    assert call(gsp=0) == _lib.ACE_ERR_INVALID_ARG
+    assert call(w=_lib.Weights(FAKE, FAKE, 0, FAKE, 0, FAKE, 0, 0, 0, 0, 0)) == _lib.ACE_ERR_INVALID_ARG
+    assert call(w=_lib.Weights(FAKE + 8, FAKE, 0, FAKE, FAKE, FAKE, 0, 0, 0, 0, 0)) == _lib.ACE_ERR_INVALID_ARG
+    assert call(ws=0) == _lib.ACE_ERR_WORKSPACE
+    assert call(ws_bytes=need - 1) == _lib.ACE_ERR_WORKSPACE
