@@ -33,6 +33,7 @@ BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
 METRIC = "MoE-layer tokens/s at 50% skip (prefill, decode); speedup vs plain top-k"
 TABLES = os.path.join(ROOT, "tests", "golden", "tables_prefill_4096_seed0.json")
 ZIPF_TABLES = os.path.join(ROOT, "tests", "golden", "tables_zipf_256_seed0.json")
+STACK_TABLES = os.path.join(ROOT, "tests", "golden", "tables_stack_48_seed0.json")
 TRAFFIC = os.path.join(ROOT, "profiles", "prefill_4096_traffic.json")
 # stage -> (kernel name in the rocprofv3 traffic record, source file)
 STAGE_KERNEL = {"gateup": ("grouped_gemm_bf16_kernel<true, 8>", "expert_gemm.hip"),
@@ -65,6 +66,11 @@ def parse():
     ap.add_argument("--decode-batches", default="1,8,32,64", help="comma-separated decode batch sizes")
     ap.add_argument("--zipf-only", action="store_true",
                     help="time only the 256-expert Zipf workload (prints its JSON, not the contract line)")
+    ap.add_argument("--stack", action="store_true",
+                    help="time only the 48-layer stack: score pass, device threshold, 8192-token prefill and "
+                         "256 decode steps at B=32 (prints its JSON, not the contract line)")
+    ap.add_argument("--stack-layers", type=int, default=0, help="layers of --stack (default: all 48)")
+    ap.add_argument("--stack-steps", type=int, default=256, help="decode steps of --stack")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="CPU oracle sample budget")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="also run one plain device copy of this many MiB (calibrates HBM byte counters)")
@@ -208,6 +214,130 @@ def main():
                                    want_plan=True)
         return fn, out
 
+    def stack_leg():
+        """48 layers of the 4096-token layer's shape (seed per layer) with a residual
+        chain x <- x + y: one score pass through the plain top-k chain, one global
+        tau from the device mapping, then the ACE chain on an 8192-token prefill and
+        on decode steps at B=32."""
+        scfg = synth.config("stack_48")
+        n_layers = args.stack_layers or synth.STACK_LAYERS
+        t0 = time.time()
+        Ws, tabs = [], []
+        for li in range(n_layers):
+            SL = synth.make_layer(scfg.with_(T=16), layer=li)
+            Ws.append({key: torch.from_numpy(SL[key]).to(dev).to(bf).contiguous()
+                       for key in ("gamma", "w_router", "w_gate", "w_up", "w_down")})
+            Ws[-1]["b_router"] = None
+            log(f"stack: layer {li} on the device ({time.time() - t0:.0f}s)")
+        # offline tables of every layer on the device (Alg. 2, Alg. 3), timed
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for li in range(n_layers):
+            r = ace.build_tables(Ws[li])
+            tabs.append((r["a_gsp"], r["a_rcr"]))
+        torch.cuda.synchronize()
+        tables_ms = (time.perf_counter() - t1) * 1e3
+        same = None
+        if os.path.exists(STACK_TABLES):  # the oracle's tables of the same layers, if stored
+            sg = json.load(open(STACK_TABLES))
+            if sg["config"]["seed"] == scfg.seed and len(sg["layers"]) >= n_layers:
+                same = sum(int(np.array_equal(tabs[li][0].cpu().numpy(), np.array(sg["layers"][li]["a_gsp"], np.float32))
+                               and np.array_equal(tabs[li][1].cpu().numpy(),
+                                                  np.array(sg["layers"][li]["a_rcr"], np.float32)))
+                           for li in range(n_layers))
+        log(f"stack: tables of {n_layers} layers in {tables_ms:.1f} ms; identical to the oracle's: {same}")
+        Ts, kk = scfg.T, scfg.k
+        x0 = torch.from_numpy(synth.make_layer(scfg, layer=0)["x"]).to(dev).to(bf)
+
+        def chain(x, tau_, skip_disable, scores=None, keep_out=None):
+            for li in range(n_layers):
+                o = {}
+                if scores is not None:
+                    o["scores"] = scores[li * x.shape[0]:(li + 1) * x.shape[0]]
+                if keep_out is not None:
+                    o["keep"] = keep_out[li]
+                r = ace.moe_forward(x, Ws[li], tabs[li][0], tabs[li][1], k=kk, tau=tau_, skip_disable=skip_disable,
+                                    write_scores=scores is not None, out=o)
+                x = x + r["y"]
+            return x
+
+        # score pass through the unskipped chain, then one global tau (App. C.1 on the device)
+        scores = torch.empty((n_layers * Ts, kk), dtype=torch.float32, device=dev)
+        chain(x0, 0.0, True, scores=scores)
+        tm = ace.tau_map(scores, [float(args.q)])
+        ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ev0.record()
+        for _ in range(5):
+            ace.tau_map(scores, [float(args.q)])
+        ev1.record()
+        torch.cuda.synchronize()
+        tau_ms = ev0.elapsed_time(ev1) / 5
+        stau = float(tm["tau"].item())
+        log(f"stack: global tau {stau} from {n_layers * Ts * kk} slots, mapping {tau_ms:.3f} ms")
+
+        keeps = torch.empty((n_layers, Ts, kk), dtype=torch.uint8, device=dev)
+
+        def timed(fn, reps):
+            fn()
+            torch.cuda.synchronize()
+            t = time.perf_counter()
+            for _ in range(reps):
+                fn()
+            torch.cuda.synchronize()
+            return (time.perf_counter() - t) / reps * 1e3
+
+        ms_ace = timed(lambda: chain(x0, stau, False, keep_out=keeps), 3)
+        per_layer = 1.0 - keeps.float().mean(dim=(1, 2)).cpu().numpy()
+        ms_top = timed(lambda: chain(x0, stau, True), 3)
+        log(f"stack prefill: ACE {ms_ace:.2f} ms, plain top-k {ms_top:.2f} ms")
+
+        B = 32
+        dkeep = torch.empty((n_layers, B, kk), dtype=torch.uint8, device=dev)
+        xs = [torch.from_numpy(synth.decode_inputs(scfg.with_(T=B), B, step)).to(dev).to(bf)
+              for step in range(args.stack_steps)]
+        dec_skip = np.zeros(n_layers)
+
+        def decode_all(skip_disable):
+            acc = torch.zeros(n_layers, device=dev)
+            for xb in xs:
+                chain(xb, stau, skip_disable, keep_out=dkeep)
+                if not skip_disable:
+                    acc += 1.0 - dkeep.float().mean(dim=(1, 2))
+            return acc
+
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        acc = decode_all(False)
+        torch.cuda.synchronize()
+        ms_dec = (time.perf_counter() - t) / len(xs) * 1e3
+        dec_skip = (acc / len(xs)).cpu().numpy()
+        t = time.perf_counter()
+        decode_all(True)
+        torch.cuda.synchronize()
+        ms_dec_top = (time.perf_counter() - t) / len(xs) * 1e3
+        res = {"workload": f"stack_48: {n_layers} MoE layers of the 4096-token layer's shape (T=8192 prefill; "
+                           f"decode B=32 x {len(xs)} steps), seed per layer, residual chain x <- x + y, "
+                           f"one global tau for skip target {args.q} from the plain top-k score pass",
+               "layers": n_layers, "tau": stau, "tau_map_ms": round(tau_ms, 4),
+               "tables_ms_all_layers": round(tables_ms, 2), "tables_identical_to_oracle_layers": same,
+               "prefill": {"ms": round(ms_ace, 3), "tokens_per_s": round(Ts / (ms_ace * 1e-3), 1),
+                           "topk_ms": round(ms_top, 3), "speedup_vs_topk": round(ms_top / ms_ace, 4),
+                           "realised_skip_overall": round(float(per_layer.mean()), 5),
+                           "realised_skip_per_layer": {"min": round(float(per_layer.min()), 5),
+                                                       "max": round(float(per_layer.max()), 5),
+                                                       "std": round(float(per_layer.std()), 5)}},
+               "decode_b32": {"ms_per_step": round(ms_dec, 3), "tokens_per_s": round(B / (ms_dec * 1e-3), 1),
+                              "topk_ms_per_step": round(ms_dec_top, 3),
+                              "speedup_vs_topk": round(ms_dec_top / ms_dec, 4),
+                              "realised_skip_per_layer": {"min": round(float(dec_skip.min()), 5),
+                                                          "max": round(float(dec_skip.max()), 5),
+                                                          "std": round(float(dec_skip.std()), 5)}},
+               "note": "times include the residual adds (torch elementwise) and host launch gaps"}
+        log(f"stack_48: {res}")
+        del Ws, scores, keeps
+        torch.cuda.empty_cache()
+        return res
+
     def zipf_leg():
         """The wider-pool layer: T=8192, 256 experts top-8 m=512, one shared expert
         (m_s=512), Zipf-skewed router bias; its own 50% threshold."""
@@ -288,6 +418,9 @@ def main():
         return
     if args.zipf_only:
         print(json.dumps({"workloads": {"zipf_256": zipf_leg()}}), flush=True)
+        return
+    if args.stack:
+        print(json.dumps({"workloads": {"stack_48": stack_leg()}}), flush=True)
         return
 
     # ---------------- prefill, ACE at the requested skip ratio

@@ -205,3 +205,41 @@ def test_zipf_256_skip_disable(zipf):
     L, D, ag, ar, gold = zipf
     r = full_check(L, D, ag, ar, gold["tau_f32"]["0.5"], skip_disable=True, tokens=ZSAMPLE[::4])
     assert r["gpu"]["keep"].all()
+
+
+# ------------------------------------------------------------------ layer stack with a residual chain and one global tau
+def test_stack_chain():
+    """Four layers of the stack (512 tokens), residual chain x <- x + y.  Score pass
+    through the plain top-k chain, one global tau from the device mapping (checked
+    against the oracle's mapping of the same scores), then the ACE chain; every
+    layer is checked against the oracle on the input the GPU chain gave it."""
+    n_layers = 4
+    cfg = synth.config("stack_48", T=512)
+    gold = make_tables.load("stack_48")
+    Ls = [synth.make_layer(cfg, layer=li) for li in range(n_layers)]
+    Ds = [device_layer(L) for L in Ls]
+    tabs = [(np.array(gold["layers"][li]["a_gsp"], np.float32), np.array(gold["layers"][li]["a_rcr"], np.float32))
+            for li in range(n_layers)]
+    x = Ds[0]["x"]
+    scores = []
+    for li in range(n_layers):
+        r = run_gpu(Ds[li], tabs[li][0], tabs[li][1], cfg.k, 0.0, x=x, skip_disable=True, write_scores=True)
+        scores.append(r["scores"])
+        x = x + torch.from_numpy(r["y"]).to(DEV).to(torch.bfloat16)
+    import paper_2609_05228_amd as ace
+    sc = torch.from_numpy(np.concatenate(scores)).to(DEV)
+    tau = float(ace.tau_map(sc, [0.5])["tau"].item())
+    want = oracle.tau.tau_table([np.asarray(s, np.float64) for s in scores], 1, [0.5])[0.5]
+    assert np.float32(want) == np.float32(tau)
+    x = Ds[0]["x"]
+    skipped = 0
+    for li in range(n_layers):
+        xl = x.float().cpu().numpy()
+        r = full_check(dict(Ls[li], x=xl), dict(Ds[li], x=x), tabs[li][0], tabs[li][1], tau,
+                       tokens=list(range(0, 512, 32)))
+        _report(f"stack layer {li} tau={tau}", r)
+        skipped += int((r["gpu"]["keep"] == 0).sum())
+        x = x + torch.from_numpy(r["gpu"]["y"]).to(DEV).to(torch.bfloat16)
+    # the chain's inputs past layer 0 differ from the score pass's (skipping changes y), so the
+    # realised ratio is near, not exactly at, the target
+    assert abs(skipped / (n_layers * 512 * cfg.k) - 0.5) < 0.02
