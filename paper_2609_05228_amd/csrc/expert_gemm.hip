@@ -18,10 +18,10 @@
 //    the row count selects one of four unrolled bodies (64..256 rows) so MFMAs
 //    and loads are issued only for the 16-row blocks a tile has;
 //  * operands move HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging)
-//    through two LDS rings: activations (L2-resident) 2-3 K stages deep, expert
-//    weights (from HBM) 5-8 stages deep, so ~80 KB of weights per CU are in
-//    flight; each wave waits only for the stage it computes next (vmcnt counted
-//    exactly from the issue schedule), then one barrier per K step;
+//    through two LDS rings in 160 KB: activations (L2-resident) 2-4 K stages deep,
+//    expert weights (from HBM) 3-8 stages deep; each wave waits only for the
+//    stage it computes next (vmcnt counted exactly from the issue schedule), then
+//    one barrier per K step;
 //  * one DMA instruction moves one MFMA fragment (16 rows x 32 k) and lane i
 //    lands at byte 16*i, which is exactly where lane i reads it back: LDS reads
 //    and writes are linear and bank-conflict free;
@@ -40,9 +40,8 @@ namespace ace {
 
 namespace {
 
-constexpr int BK = 64;               // K per stage
 constexpr int kFragBytes = 1024;     // one MFMA fragment: 16 rows x 32 bf16
-constexpr int kLdsBytes = 144 * 1024;
+constexpr int kLdsBytes = 160 * 1024;
 
 struct TileInfo {
   int e, row0, rows;
@@ -116,21 +115,32 @@ __device__ __forceinline__ void wait_vmcnt(int n) {
 }
 
 constexpr int kWaves = 8;  // waves per workgroup (two per SIMD)
+// 32-wide k halves per pipeline stage.  Two (64-wide stages) measured faster than
+// one with deeper rings: the stream rate, not the bytes in flight, is the limit.
+template <int CG> constexpr int stage_halves() { return 2; }
 
-// Pipeline geometry for a tile of MB 16-row blocks (MB a multiple of 4) and CG
+// Pipeline geometry for a tile of MB 16-row blocks (MB a multiple of 4), CG
 // column groups (gate/up: 16 features each, a gate and an up block; down: 32
-// output columns, two blocks).  A (activation rows, mostly L2 hits) and B
-// (expert weights, streamed from HBM) have their own LDS rings within 144 KB.
-template <int MB, int CG> struct Pipe {
-  static constexpr int NA = MB / 4;                 // A DMAs per wave per stage (2*MB per workgroup)
-  static constexpr int NB = CG / 2;                 // B DMAs per wave per stage (4*CG per workgroup)
-  static constexpr int ASZ = 2 * MB * kFragBytes;   // A stage: MB row blocks x 2 k halves
-  static constexpr int BSZ = 4 * CG * kFragBytes;   // B stage: 2*CG column blocks x 2 k halves
-  static constexpr int SA = (MB >= 16 || (CG == 8 && MB >= 8)) ? 2 : MB >= 8 ? 3 : 4;
+// output columns, two blocks) and KH 32-wide k halves per stage (BK = 32 KH).
+// A (activation rows, mostly L2 hits) and B (expert weights, streamed from HBM)
+// have their own LDS rings.  A stage of A holds MB*KH fragments spread over the
+// 8 waves (a wave stages na <= NA_MAX of them); a stage of B holds 2*CG*KH
+// fragments, NB per wave.
+template <int MB, int CG, int KH> struct Pipe {
+  static constexpr int BK = 32 * KH;
+  static constexpr int FA = MB * KH;                      // A fragments per stage
+  static constexpr int NA_MAX = (FA + kWaves - 1) / kWaves;
+  static constexpr int NB = 2 * CG * KH / kWaves;         // B DMAs per wave per stage
+  static constexpr int ASZ = FA * kFragBytes;
+  static constexpr int BSZ = 2 * CG * KH * kFragBytes;
+  static constexpr int SA = KH == 2 ? ((MB >= 16 || (CG >= 8 && MB >= 8)) ? 2 : MB >= 8 ? 3 : 4) : 4;
   static constexpr int SB0 = (kLdsBytes - SA * ASZ) / BSZ;
-  static constexpr int SB = SB0 > 8 ? 8 : SB0;
+  static constexpr int SBMAX = KH == 2 ? 8 : 10;
+  static constexpr int SB = SB0 > SBMAX ? SBMAX : SB0;
+  static_assert(2 * CG * KH % kWaves == 0, "B fragments must spread evenly over the waves");
   static_assert(SB >= 2 && SA >= 2, "ring too shallow");
-  static_assert((SA - 1) * NA + (SB - 1) * NB + NA + NB <= 31, "outstanding DMAs exceed the wait table");
+  static_assert(SA * ASZ + SB * BSZ <= kLdsBytes, "rings exceed LDS");
+  static_assert((SA - 1) * NA_MAX + (SB - 1) * NB + NA_MAX + NB <= 31, "outstanding DMAs exceed the wait table");
 };
 
 // This wave's DMA issue sequence: a prologue of B stages 0..PB-1 then A stages
@@ -138,68 +148,74 @@ template <int MB, int CG> struct Pipe {
 // A(j+SA-1) and then B(j+SB-1), each only if it exists.  cum_ops(j) = DMAs
 // issued before iteration j.
 template <class P>
-__device__ __forceinline__ int cum_ops(int j, int nk) {
+__device__ __forceinline__ int cum_ops(int j, int nk, int na) {
   const int PB = min(P::SB - 1, nk), PA = min(P::SA - 1, nk);
-  return PB * P::NB + PA * P::NA + max(0, min(j, nk - P::SA + 1)) * P::NA +
-         max(0, min(j, nk - P::SB + 1)) * P::NB;
+  return PB * P::NB + PA * na + max(0, min(j, nk - P::SA + 1)) * na + max(0, min(j, nk - P::SB + 1)) * P::NB;
 }
 
 // DMAs that may still be outstanding at the wait before stage kt's compute:
 // everything issued after the later of A(kt) and B(kt) (vmcnt completes in
-// issue order).
+// issue order).  na = this wave's A DMAs per stage.
 template <class P>
-__device__ __forceinline__ int pending_ok(int kt, int nk) {
+__device__ __forceinline__ int pending_ok(int kt, int nk, int na) {
   const int PB = min(P::SB - 1, nk), PA = min(P::SA - 1, nk);
   int end_a, end_b;
-  if (kt < PA) {
-    end_a = PB * P::NB + (kt + 1) * P::NA;
+  if (na == 0) {
+    end_a = 0;  // this wave stages no A fragments
+  } else if (kt < PA) {
+    end_a = PB * P::NB + (kt + 1) * na;
   } else {
-    end_a = cum_ops<P>(kt - P::SA + 1, nk) + P::NA;
+    end_a = cum_ops<P>(kt - P::SA + 1, nk, na) + na;
   }
   if (kt < PB) {
     end_b = (kt + 1) * P::NB;
   } else {
     const int i = kt - P::SB + 1;
-    end_b = cum_ops<P>(i, nk) + (i + P::SA - 1 < nk ? P::NA : 0) + P::NB;
+    end_b = cum_ops<P>(i, nk, na) + (i + P::SA - 1 < nk ? na : 0) + P::NB;
   }
-  return cum_ops<P>(kt, nk) - max(end_a, end_b);
+  return cum_ops<P>(kt, nk, na) - max(end_a, end_b);
 }
 
-// One M tile x one N tile with MB 16-row blocks and CG column groups.  The B
-// stage holds 4*CG fragments b = 4 fg + 2 cb + h: column group fg, block cb
-// (gate/up: cb 0 gate, 1 up; down: the group's two 16-column halves), k half h.
-// Wave w stages A fragments w, w+8, ... and B fragments w*NB .. w*NB+NB-1, and
-// computes row blocks wr, wr+4, ... (wr = w/2) against the CG/2 column groups
-// starting at wc*CG/2 (wc = w%2).
-template <bool GATEUP, int MB, int CG>
+// One M tile x one N tile with MB 16-row blocks, CG column groups and KH k
+// halves per stage.  A stage of A holds fragments f = rb*KH + h (row block rb,
+// k half h); wave w stages f = w, w+8, ... .  A stage of B holds 2*CG*KH
+// fragments b = (2 fg + cb)*KH + h: column group fg, block cb (gate/up: cb 0
+// gate, 1 up; down: the group's two 16-column halves), k half h; wave w stages
+// b = w*NB .. w*NB+NB-1.  Wave w computes row blocks wr, wr+4, ... (wr = w/2)
+// against the CG/2 column groups starting at wc*CG/2 (wc = w%2).
+template <bool GATEUP, int MB, int CG, int KH>
 __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, uint8_t *smem) {
-  using P = Pipe<MB, CG>;
-  constexpr int NA = P::NA, NB = P::NB, SA = P::SA, SB = P::SB;
+  using P = Pipe<MB, CG, KH>;
+  constexpr int NAM = P::NA_MAX, NB = P::NB, SA = P::SA, SB = P::SB, BK = P::BK;
   constexpr int MW = MB / 4;   // row blocks per wave
   constexpr int CW = CG / 2;   // column groups per wave
   constexpr int BN = GATEUP ? 16 * CG : 32 * CG;  // tile width (features or output columns)
 
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const int wr = wave >> 1, wc = wave & 1;
   const int K = GATEUP ? a.d : a.m;
   const bf16_t *act = static_cast<const bf16_t *>(a.act);
+  // A fragments this wave stages per stage (wave-uniform)
+  const int na = P::FA > wave ? (P::FA - wave + kWaves - 1) / kWaves : 0;
 
-  // A fragments this wave stages: f = wave + 8 j -> row block f / 2, k half f % 2
-  const bf16_t *asrc[NA];
+  // A fragments this wave stages: f = wave + 8 j -> row block f / KH, k half f % KH
+  const bf16_t *asrc[NAM];
 #pragma unroll
-  for (int j = 0; j < NA; ++j) {
-    const int f = wave + kWaves * j;
-    const int row = min((f >> 1) * 16 + r16, ti.rows - 1);  // rows past the tile repeat its last row
+  for (int j = 0; j < NAM; ++j) {
+    const int f = min(wave + kWaves * j, P::FA - 1);
+    const int row = min((f / KH) * 16 + r16, ti.rows - 1);  // rows past the tile repeat its last row
     const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
-    asrc[j] = act + static_cast<size_t>(src_row) * K + (f & 1) * 32 + 8 * g;
+    asrc[j] = act + static_cast<size_t>(src_row) * K + (f % KH) * 32 + 8 * g;
   }
   // B fragments this wave stages: b = wave * NB + t
   const bf16_t *bsrc[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t) {
     const int b = wave * NB + t;
-    const int fg = b >> 2, cb = (b >> 1) & 1, h = b & 1;
+    const int blk = b / KH, h = b % KH;
+    const int fg = blk >> 1, cb = blk & 1;
     if (GATEUP) {
       const size_t f = static_cast<size_t>(ti.e) * a.m + nt * BN + fg * 16 + r16;
       bsrc[t] = static_cast<const bf16_t *>(cb ? a.w1 : a.w0) + f * a.d + 32 * h + 8 * g;
@@ -229,17 +245,19 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   for (int s = 0; s < SA - 1 && s < nk; ++s) {
     const uint32_t st = ldsA + s * P::ASZ;
 #pragma unroll
-    for (int j = 0; j < NA; ++j) dma16(asrc[j] + s * BK, st + (wave + kWaves * j) * kFragBytes);
+    for (int j = 0; j < NAM; ++j)
+      if (j < na) dma16(asrc[j] + s * BK, st + (wave + kWaves * j) * kFragBytes);
   }
 
   for (int kt = 0; kt < nk; ++kt) {
-    wait_vmcnt(pending_ok<P>(kt, nk));
+    wait_vmcnt(pending_ok<P>(kt, nk, na));
     barrier();  // stage kt landed for every wave; every wave is done with stage kt-1
     if (kt + SA - 1 < nk) {
       const int s = kt + SA - 1;
       const uint32_t st = ldsA + (s % SA) * P::ASZ;
 #pragma unroll
-      for (int j = 0; j < NA; ++j) dma16(asrc[j] + s * BK, st + (wave + kWaves * j) * kFragBytes);
+      for (int j = 0; j < NAM; ++j)
+        if (j < na) dma16(asrc[j] + s * BK, st + (wave + kWaves * j) * kFragBytes);
     }
     if (kt + SB - 1 < nk) {
       const int s = kt + SB - 1;
@@ -250,15 +268,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     const uint8_t *sa = smemA + (kt % SA) * P::ASZ;
     const uint8_t *sb = smemB + (kt % SB) * P::BSZ;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < KH; ++h) {
       bf16x8_t bf[2 * CW];  // [fl * 2 + cb]: column group wc*CW + fl, block cb
 #pragma unroll
       for (int c = 0; c < 2 * CW; ++c)
-        bf[c] = *reinterpret_cast<const bf16x8_t *>(sb + ((wc * CW + (c >> 1)) * 4 + (c & 1) * 2 + h) * kFragBytes +
+        bf[c] = *reinterpret_cast<const bf16x8_t *>(sb + ((2 * (wc * CW + (c >> 1)) + (c & 1)) * KH + h) * kFragBytes +
                                                     16 * lane);
 #pragma unroll
       for (int i = 0; i < MW; ++i) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t *>(sa + (2 * (wr + 4 * i) + h) * kFragBytes + 16 * lane);
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t *>(sa + ((wr + 4 * i) * KH + h) * kFragBytes + 16 * lane);
 #pragma unroll
         for (int c = 0; c < 2 * CW; ++c)
           acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bf[c], acc[i][c], 0, 0, 0);
@@ -313,13 +331,13 @@ __global__ __launch_bounds__(kWaves * 64) void grouped_gemm_bf16_kernel(GemmArgs
   __shared__ __align__(16) uint8_t smem[kLdsBytes];
   const int blocks = (ti.rows + 15) >> 4;
   if (blocks <= 4)
-    gemm_tile<GATEUP, 4, CG>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 4, CG, stage_halves<CG>()>(a, ti, nt, smem);
   else if (blocks <= 8)
-    gemm_tile<GATEUP, 8, CG>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 8, CG, stage_halves<CG>()>(a, ti, nt, smem);
   else if (blocks <= 12)
-    gemm_tile<GATEUP, 12, CG>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 12, CG, stage_halves<CG>()>(a, ti, nt, smem);
   else
-    gemm_tile<GATEUP, 16, CG>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 16, CG, stage_halves<CG>()>(a, ti, nt, smem);
 }
 
 // ------------------------------------------------------------------ fp32 (tiled FMA)
