@@ -243,3 +243,47 @@ def test_stack_chain():
     # the chain's inputs past layer 0 differ from the score pass's (skipping changes y), so the
     # realised ratio is near, not exactly at, the target
     assert abs(skipped / (n_layers * 512 * cfg.k) - 0.5) < 0.02
+
+
+# ------------------------------------------------------------------ edge shapes and degenerate settings
+EDGE = [
+    # name, config overrides, tau choice, m_min
+    ("d16384", dict(T=100, d=16384, N=16, k=4, m=64, seed=11), 0.4, 1),       # largest hidden size
+    ("N256_k8_T33", dict(T=33, d=256, N=256, k=8, m=64, seed=12), 0.5, 1),   # widest pool, small batch
+    ("k1", dict(T=90, d=128, N=8, k=1, m=64, seed=13), 0.5, 1),              # top-1: nothing skippable
+    ("k_eq_N", dict(T=70, d=128, N=4, k=4, m=128, seed=14), 0.5, 1),         # every expert routed
+    ("mmin_eq_k", dict(T=80, d=256, N=16, k=4, m=64, seed=15), 0.5, 4),      # safeguard keeps all
+    ("T_ragged_1000", dict(T=1000, d=256, N=32, k=6, m=192, seed=16), 0.3, 2),
+]
+
+
+@pytest.mark.parametrize("case", EDGE, ids=lambda c: c[0])
+def test_edge_shapes(case):
+    name, kw, q, m_min = case
+    L = synth.make_layer(synth.config("prefill_4096", **kw))
+    # the tables are inputs of the layer: seeded positive per-expert values stand in
+    # (the oracle's GSP forms [d, d] products, too large at d = 16384)
+    rng = np.random.default_rng(kw["seed"])
+    N = L["cfg"].N
+    tb = {"a_gsp": rng.uniform(0.5, 1.5, N).astype(np.float32), "a_rcr": rng.uniform(0.5, 1.5, N).astype(np.float32)}
+    tau = _taus(L, tb["a_gsp"], tb["a_rcr"], [q], m_min)[q]
+    toks = None if L["cfg"].T <= 100 else list(range(0, L["cfg"].T, 7))
+    r = full_check(L, device_layer(L), tb["a_gsp"], tb["a_rcr"], tau, m_min=m_min, tokens=toks)
+    _report(f"edge {name} tau={tau}", r)
+    keep = r["gpu"]["keep"].astype(bool)
+    assert keep[:, 0].all() and (keep.sum(1) >= m_min).all()
+    if m_min == L["cfg"].k or L["cfg"].k == 1:
+        assert keep.all()
+
+
+@pytest.mark.parametrize("tau", [0.0, -1.0, float("inf")])
+def test_tau_extremes(tiny, tau):
+    """tau <= 0 skips nothing (gates scaled by 1/(1+eps)); +inf skips every slot but the top-1."""
+    L, D, ag, ar = tiny
+    r = full_check(L, D, ag, ar, tau)
+    keep = r["gpu"]["keep"].astype(bool)
+    if tau <= 0:
+        assert keep.all()
+        assert np.allclose(r["gpu"]["gates"], r["oracle"]["g"] / (1 + 1e-6), rtol=2e-6, atol=2e-7)
+    else:
+        assert keep[:, 0].all() and not keep[:, 1:].any()
