@@ -296,6 +296,7 @@ __global__ __launch_bounds__(256) void route_partial_kernel(RouteArgs a) {
   const int t0 = blockIdx.x * kTok;
   const int s = blockIdx.y;
   const int nbs = (a.d >> 5) / a.ksplit;  // blocks per slice
+  if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) a.ticket[0] = 0u;  // for the select kernel's plan
   wave_logits<T, NT, NP + 1>(a, t0, s * nbs + wave, (s + 1) * nbs, kPartWaves, zred[wave], ssred[wave]);
   __syncthreads();
   const size_t plane = static_cast<size_t>(s) * a.T;
@@ -313,6 +314,95 @@ __global__ __launch_bounds__(256) void route_partial_kernel(RouteArgs a) {
 #pragma unroll
     for (int w = 0; w < kPartWaves; ++w) ss += ssred[w][tid];
     a.sspart[plane + t0 + tid] = ss;
+  }
+}
+
+// Small batches (at most 16 chunks): the select workgroup that finishes last
+// writes the whole dispatch plan, so no plan kernels follow.  Each workgroup
+// publishes its chunk (counts, ranks, routing) with a device-scope fence before
+// taking a ticket; the last one fences again (its L1 then holds no stale lines)
+// and computes, from integers only: counts, their exclusive scan (offsets), the
+// M-tile list, and row = offsets[e] + (kept slots of e in earlier chunks) +
+// rank for every kept slot.  The result does not depend on which workgroup is
+// last.
+__device__ __forceinline__ void plan_if_last(const RouteArgs &a) {
+  __shared__ int last;
+  __shared__ int cnt[kMaxN], off[kMaxN + 1], tcnt[kMaxN], toff[kMaxN + 1];
+  __shared__ int base[kRouteMaxSplitChunks][kMaxN];  // kept slots of e in chunks before g
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int N = a.N, G = gridDim.x;
+  __threadfence();
+  __syncthreads();
+  if (tid == 0) last = atomicAdd(a.ticket, 1u) == static_cast<uint32_t>(G - 1);
+  __syncthreads();
+  if (!last) return;
+  __threadfence();
+  for (int e = tid; e < N; e += 512) {
+    int run = 0;
+    for (int g = 0; g < G; ++g) {
+      base[g][e] = run;
+      run += a.chunk_count[static_cast<size_t>(g) * N + e];
+    }
+    cnt[e] = run;
+    tcnt[e] = (run + kTileM - 1) / kTileM;
+  }
+  __syncthreads();
+  if (tid < 64) {
+    // exclusive scans of the counts and tile counts (N <= 256: four per lane)
+    int s = 0, st = 0, loc[4], loct[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = lane * 4 + j;
+      loc[j] = s;
+      loct[j] = st;
+      s += e < N ? cnt[e] : 0;
+      st += e < N ? tcnt[e] : 0;
+    }
+    int inc = s, inct = st;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(inc, o), vt = __shfl_up(inct, o);
+      if (lane >= o) {
+        inc += v;
+        inct += vt;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = lane * 4 + j;
+      if (e < N) {
+        off[e] = inc - s + loc[j];
+        toff[e] = inct - st + loct[j];
+      }
+    }
+    if (lane == 63) {
+      off[N] = inc;
+      toff[N] = inct;
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < N; e += 512) {
+    a.counts[e] = cnt[e];
+    a.offsets[e] = off[e];
+    for (int j = 0; j < tcnt[e]; ++j) {
+      const int tg = toff[e] + j;
+      a.tile_expert[tg] = e;
+      a.tile_row0[tg] = off[e] + j * kTileM;
+      a.tile_rows[tg] = min(kTileM, cnt[e] - j * kTileM);
+    }
+  }
+  if (tid == 0) {
+    a.offsets[N] = off[N];
+    a.n_tiles[0] = toff[N];
+  }
+  const int slots = a.T * a.k;
+  for (int o = tid; o < slots; o += 512) {
+    if (!a.keep[o]) continue;
+    const int t = o / a.k;
+    const int e = a.topk_idx[o];
+    const int row = off[e] + base[t / kTok][e] + a.local_rank[o];
+    a.perm[row] = t;
+    a.slot_row[o] = row;
   }
 }
 
@@ -512,6 +602,7 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   }
   for (int e = tid; e < N; e += 512)
     a.chunk_count[static_cast<size_t>(blockIdx.x) * N + e] = static_cast<uint8_t>(__popc(emask[e]));
+  if constexpr (SPLIT) plan_if_last(a);
 }
 
 template <typename T, int NT>
