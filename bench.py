@@ -393,6 +393,26 @@ def main():
         log(f"calibration copy of {args.calib_copy_mb} MiB done")
         del src, dst
 
+    def graph_ms(fn, steps):
+        """ms per step of `fn` captured once in a HIP graph and replayed (no host launch cost)."""
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            fn()
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            fn()
+        for _ in range(3):
+            g.replay()
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for _ in range(steps):
+            g.replay()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) / steps * 1e3
+
     def decode_legs():
         """Decode batches through the same layer, tau transferred from prefill."""
         dec = {}
@@ -402,12 +422,16 @@ def main():
             s_top, _ = make_step(xb, True, tau)
             ms_a = time_steps(s_ace, max(args.steps, 50), args.warmup, torch)
             ms_t = time_steps(s_top, max(args.steps, 50), args.warmup, torch)
+            ms_ga, ms_gt = graph_ms(s_ace, max(args.steps, 50)), graph_ms(s_top, max(args.steps, 50))
             kb = o_ace["keep"].cpu().numpy()
             ea = int((o_ace["counts"].cpu().numpy() > 0).sum())
             bb, _ = layer_bytes(B, d, N, k, m, ea, int(kb.sum()))
             dec[str(B)] = {"tokens_per_s": round(B / (ms_a * 1e-3), 1), "ms_per_step": round(ms_a, 4),
                            "topk_ms_per_step": round(ms_t, 4), "speedup_vs_topk": round(ms_t / ms_a, 4),
-                           "realised_skip": round(1 - kb.mean(), 4), "experts_active": ea,
+                           "graph_ms_per_step": round(ms_ga, 4), "graph_topk_ms_per_step": round(ms_gt, 4),
+                           "graph_tokens_per_s": round(B / (ms_ga * 1e-3), 1),
+                           "graph_speedup_vs_topk": round(ms_gt / ms_ga, 4),
+                           "realised_skip": round(float(1 - kb.mean()), 4), "experts_active": ea,
                            "alg_gbs": round(bb / (ms_a * 1e-3) / 1e9, 1),
                            "hbm_frac": round(bb / (ms_a * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
             log(f"decode B={B}: {dec[str(B)]}")
