@@ -22,9 +22,9 @@
 //    expert weights (from HBM) 3-8 stages deep; each wave waits only for the
 //    stage it computes next (vmcnt counted exactly from the issue schedule), then
 //    one barrier per K step;
-//  * one DMA instruction moves one MFMA fragment (16 rows x 32 k) and lane i
-//    lands at byte 16*i, which is exactly where lane i reads it back: LDS reads
-//    and writes are linear and bank-conflict free;
+//  * one DMA instruction moves 8 rows x 128 bytes (whole cache lines) and lane i
+//    lands at byte 16*i; the chunk a lane fetches is XOR-swizzled by its row so
+//    the MFMA fragment reads (16 rows x 16 bytes) are bank-conflict free;
 //  * 8 waves (two per SIMD, so one wave's LDS reads overlap the other's MFMAs)
 //    as 4 x 2: a wave owns a quarter of the row blocks (interleaved, so short
 //    tiles stay balanced) and two column groups (gate/up: gate and up blocks of
@@ -95,7 +95,7 @@ __device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
 
 __device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
 
-// wait until at most n (0..31) of this wave's vector memory operations are outstanding
+// wait until at most n (0..63) of this wave's vector memory operations are outstanding
 __device__ __forceinline__ void wait_vmcnt(int n) {
 #define ACE_VMCNT_CASE(c) \
   case c:                 \
@@ -108,13 +108,19 @@ __device__ __forceinline__ void wait_vmcnt(int n) {
     ACE_VMCNT_CASE(15) ACE_VMCNT_CASE(16) ACE_VMCNT_CASE(17) ACE_VMCNT_CASE(18) ACE_VMCNT_CASE(19)
     ACE_VMCNT_CASE(20) ACE_VMCNT_CASE(21) ACE_VMCNT_CASE(22) ACE_VMCNT_CASE(23) ACE_VMCNT_CASE(24)
     ACE_VMCNT_CASE(25) ACE_VMCNT_CASE(26) ACE_VMCNT_CASE(27) ACE_VMCNT_CASE(28) ACE_VMCNT_CASE(29)
-    ACE_VMCNT_CASE(30) ACE_VMCNT_CASE(31)
+    ACE_VMCNT_CASE(30) ACE_VMCNT_CASE(31) ACE_VMCNT_CASE(32) ACE_VMCNT_CASE(33) ACE_VMCNT_CASE(34)
+    ACE_VMCNT_CASE(35) ACE_VMCNT_CASE(36) ACE_VMCNT_CASE(37) ACE_VMCNT_CASE(38) ACE_VMCNT_CASE(39)
+    ACE_VMCNT_CASE(40) ACE_VMCNT_CASE(41) ACE_VMCNT_CASE(42) ACE_VMCNT_CASE(43) ACE_VMCNT_CASE(44)
+    ACE_VMCNT_CASE(45) ACE_VMCNT_CASE(46) ACE_VMCNT_CASE(47) ACE_VMCNT_CASE(48) ACE_VMCNT_CASE(49)
+    ACE_VMCNT_CASE(50) ACE_VMCNT_CASE(51) ACE_VMCNT_CASE(52) ACE_VMCNT_CASE(53) ACE_VMCNT_CASE(54)
+    ACE_VMCNT_CASE(55) ACE_VMCNT_CASE(56) ACE_VMCNT_CASE(57) ACE_VMCNT_CASE(58) ACE_VMCNT_CASE(59)
+    ACE_VMCNT_CASE(60) ACE_VMCNT_CASE(61) ACE_VMCNT_CASE(62) ACE_VMCNT_CASE(63)
     default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
   }
 #undef ACE_VMCNT_CASE
 }
 
-constexpr int kWaves = 8;  // waves per workgroup (two per SIMD)
+constexpr int kGemmWaves = 8;  // waves per workgroup (two per SIMD)
 // 32-wide k halves per pipeline stage.  Two (64-wide stages) measured faster than
 // one with deeper rings: the stream rate, not the bytes in flight, is the limit.
 template <int CG> constexpr int stage_halves() { return 2; }
@@ -126,21 +132,21 @@ template <int CG> constexpr int stage_halves() { return 2; }
 // have their own LDS rings.  A stage of A holds MB*KH fragments spread over the
 // 8 waves (a wave stages na <= NA_MAX of them); a stage of B holds 2*CG*KH
 // fragments, NB per wave.
-template <int MB, int CG, int KH> struct Pipe {
+template <int MB, int CG, int KH, int W> struct Pipe {
   static constexpr int BK = 32 * KH;
   static constexpr int FA = MB * KH;                      // A fragments per stage
-  static constexpr int NA_MAX = (FA + kWaves - 1) / kWaves;
-  static constexpr int NB = 2 * CG * KH / kWaves;         // B DMAs per wave per stage
+  static constexpr int NA_MAX = (FA + W - 1) / W;
+  static constexpr int NB = 2 * CG * KH / W;              // B DMAs per wave per stage
   static constexpr int ASZ = FA * kFragBytes;
   static constexpr int BSZ = 2 * CG * KH * kFragBytes;
   static constexpr int SA = KH == 2 ? ((MB >= 16 || (CG >= 8 && MB >= 8)) ? 2 : MB >= 8 ? 3 : 4) : 4;
   static constexpr int SB0 = (kLdsBytes - SA * ASZ) / BSZ;
   static constexpr int SBMAX = KH == 2 ? 8 : 10;
   static constexpr int SB = SB0 > SBMAX ? SBMAX : SB0;
-  static_assert(2 * CG * KH % kWaves == 0, "B fragments must spread evenly over the waves");
+  static_assert(2 * CG * KH % W == 0, "B fragments must spread evenly over the waves");
   static_assert(SB >= 2 && SA >= 2, "ring too shallow");
   static_assert(SA * ASZ + SB * BSZ <= kLdsBytes, "rings exceed LDS");
-  static_assert((SA - 1) * NA_MAX + (SB - 1) * NB + NA_MAX + NB <= 31, "outstanding DMAs exceed the wait table");
+  static_assert((SA - 1) * NA_MAX + (SB - 1) * NB + NA_MAX + NB <= 63, "outstanding DMAs exceed the wait table");
 };
 
 // This wave's DMA issue sequence: a prologue of B stages 0..PB-1 then A stages
@@ -176,54 +182,70 @@ __device__ __forceinline__ int pending_ok(int kt, int nk, int na) {
   return cum_ops<P>(kt, nk, na) - max(end_a, end_b);
 }
 
-// One M tile x one N tile with MB 16-row blocks, CG column groups and KH k
-// halves per stage.  A stage of A holds fragments f = rb*KH + h (row block rb,
-// k half h); wave w stages f = w, w+8, ... .  A stage of B holds 2*CG*KH
-// fragments b = (2 fg + cb)*KH + h: column group fg, block cb (gate/up: cb 0
-// gate, 1 up; down: the group's two 16-column halves), k half h; wave w stages
-// b = w*NB .. w*NB+NB-1.  Wave w computes row blocks wr, wr+4, ... (wr = w/2)
-// against the CG/2 column groups starting at wc*CG/2 (wc = w%2).
-template <bool GATEUP, int MB, int CG, int KH>
+// One M tile x one N tile with MB 16-row blocks, CG column groups and KH = 2
+// k halves per stage (64-wide stages: 128 bytes of every row).  One DMA
+// instruction moves an 8-row unit: 8 rows x 128 bytes, each row a whole cache
+// line (16-row x 64-byte fragments touch twice as many lines per instruction and
+// stream measurably slower).  A stage of A holds units u = 2 rb + j (row block
+// rb, row half j), wave w staging u = w, w+W, ...; a stage of B holds units
+// b = 2 (2 fg + cb) + j (column group fg, block cb (gate/up: 0 gate, 1 up;
+// down: the group's two 16-column halves), row half j), wave w staging
+// b = w*NB .. w*NB+NB-1.  Inside a unit, row r's 16-byte chunk c sits in slot
+// c ^ r ^ j, so the MFMA fragment reads (16 rows, one chunk each) hit distinct
+// banks.  Wave w computes row blocks wr, wr+RW, ... (wr = w/2) against the CG/2
+// column groups starting at wc*CG/2 (wc = w%2).
+template <bool GATEUP, int MB, int CG, int KH, int W>
 __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, uint8_t *smem) {
-  using P = Pipe<MB, CG, KH>;
+  static_assert(KH == 2, "8-row DMA units span a 64-wide K stage");
+  using P = Pipe<MB, CG, KH, W>;
+  constexpr int RW = W / 2;    // waves along the rows
   constexpr int NAM = P::NA_MAX, NB = P::NB, SA = P::SA, SB = P::SB, BK = P::BK;
-  constexpr int MW = MB / 4;   // row blocks per wave
+  constexpr int MW = MB / RW;  // row blocks per wave
   constexpr int CW = CG / 2;   // column groups per wave
   constexpr int BN = GATEUP ? 16 * CG : 32 * CG;  // tile width (features or output columns)
-
+  static_assert(NB % 2 == 0 && W % 2 == 0, "a wave's units must keep one row half");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g = lane >> 4;
   const int wr = wave >> 1, wc = wave & 1;
   const int K = GATEUP ? a.d : a.m;
   const bf16_t *act = static_cast<const bf16_t *>(a.act);
-  // A fragments this wave stages per stage (wave-uniform)
-  const int na = P::FA > wave ? (P::FA - wave + kWaves - 1) / kWaves : 0;
+  // A units this wave stages per stage (wave-uniform)
+  const int na = P::FA > wave ? (P::FA - wave + W - 1) / W : 0;
+  // DMA lane -> (row in unit, source chunk): the lane lands in slot lane & 7 of row lane >> 3
+  const int ur = lane >> 3;
+  const int uc0 = (lane & 7) ^ ur;  // chunk for row half 0; half 1 flips bit 0
 
-  // A fragments this wave stages: f = wave + 8 j -> row block f / KH, k half f % KH
+  // A units this wave stages: u = wave + W j -> row block u / 2, row half u % 2 (= wave % 2)
   const bf16_t *asrc[NAM];
 #pragma unroll
   for (int j = 0; j < NAM; ++j) {
-    const int f = min(wave + kWaves * j, P::FA - 1);
-    const int row = min((f / KH) * 16 + r16, ti.rows - 1);  // rows past the tile repeat its last row
+    const int u = min(wave + W * j, P::FA - 1);
+    const int row = min((u >> 1) * 16 + (u & 1) * 8 + ur, ti.rows - 1);  // rows past the tile repeat its last row
     const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
-    asrc[j] = act + static_cast<size_t>(src_row) * K + (f % KH) * 32 + 8 * g;
+    asrc[j] = act + static_cast<size_t>(src_row) * K + 8 * (uc0 ^ (u & 1));
   }
-  // B fragments this wave stages: b = wave * NB + t
+  // B units this wave stages: b = wave * NB + t -> block b / 2, row half t % 2
   const bf16_t *bsrc[NB];
 #pragma unroll
   for (int t = 0; t < NB; ++t) {
     const int b = wave * NB + t;
-    const int blk = b / KH, h = b % KH;
+    const int blk = b >> 1, j = b & 1;
     const int fg = blk >> 1, cb = blk & 1;
+    const int c = 8 * (uc0 ^ j);
     if (GATEUP) {
-      const size_t f = static_cast<size_t>(ti.e) * a.m + nt * BN + fg * 16 + r16;
-      bsrc[t] = static_cast<const bf16_t *>(cb ? a.w1 : a.w0) + f * a.d + 32 * h + 8 * g;
+      const size_t f = static_cast<size_t>(ti.e) * a.m + nt * BN + fg * 16 + 8 * j + ur;
+      bsrc[t] = static_cast<const bf16_t *>(cb ? a.w1 : a.w0) + f * a.d + c;
     } else {
-      const size_t n = static_cast<size_t>(ti.e) * a.d + nt * BN + fg * 32 + cb * 16 + r16;
-      bsrc[t] = static_cast<const bf16_t *>(a.w0) + n * a.m + 32 * h + 8 * g;
+      const size_t n = static_cast<size_t>(ti.e) * a.d + nt * BN + fg * 32 + cb * 16 + 8 * j + ur;
+      bsrc[t] = static_cast<const bf16_t *>(a.w0) + n * a.m + c;
     }
   }
+  // fragment read offsets inside a 16-row block (two units) for k half h:
+  // row r16 sits in unit half r16 / 8, its chunk 4h + g in slot (4h + g) ^ (r16 % 8) ^ (r16 / 8)
+  const int rlo = r16 & 7, uh = r16 >> 3;
+  const int rd_off0 = uh * kFragBytes + rlo * 128 + ((g ^ rlo ^ uh) << 4);
+  const int rd_off1 = uh * kFragBytes + rlo * 128 + (((4 + g) ^ rlo ^ uh) << 4);
   const uint32_t ldsA = lds_addr(smem);
   const uint32_t ldsB = ldsA + SA * P::ASZ;
   const uint8_t *smemA = smem;
@@ -246,7 +268,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     const uint32_t st = ldsA + s * P::ASZ;
 #pragma unroll
     for (int j = 0; j < NAM; ++j)
-      if (j < na) dma16(asrc[j] + s * BK, st + (wave + kWaves * j) * kFragBytes);
+      if (j < na) dma16(asrc[j] + s * BK, st + (wave + W * j) * kFragBytes);
   }
 
   for (int kt = 0; kt < nk; ++kt) {
@@ -257,7 +279,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       const uint32_t st = ldsA + (s % SA) * P::ASZ;
 #pragma unroll
       for (int j = 0; j < NAM; ++j)
-        if (j < na) dma16(asrc[j] + s * BK, st + (wave + kWaves * j) * kFragBytes);
+        if (j < na) dma16(asrc[j] + s * BK, st + (wave + W * j) * kFragBytes);
     }
     if (kt + SB - 1 < nk) {
       const int s = kt + SB - 1;
@@ -272,11 +294,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       bf16x8_t bf[2 * CW];  // [fl * 2 + cb]: column group wc*CW + fl, block cb
 #pragma unroll
       for (int c = 0; c < 2 * CW; ++c)
-        bf[c] = *reinterpret_cast<const bf16x8_t *>(sb + ((2 * (wc * CW + (c >> 1)) + (c & 1)) * KH + h) * kFragBytes +
-                                                    16 * lane);
+        bf[c] = *reinterpret_cast<const bf16x8_t *>(sb + (2 * (wc * CW + (c >> 1)) + (c & 1)) * 2 * kFragBytes +
+                                                    (h ? rd_off1 : rd_off0));
 #pragma unroll
       for (int i = 0; i < MW; ++i) {
-        const bf16x8_t av = *reinterpret_cast<const bf16x8_t *>(sa + ((wr + 4 * i) * KH + h) * kFragBytes + 16 * lane);
+        const bf16x8_t av =
+            *reinterpret_cast<const bf16x8_t *>(sa + (wr + RW * i) * 2 * kFragBytes + (h ? rd_off1 : rd_off0));
 #pragma unroll
         for (int c = 0; c < 2 * CW; ++c)
           acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bf[c], acc[i][c], 0, 0, 0);
@@ -295,7 +318,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       for (int i = 0; i < MW; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int row = (wr + 4 * i) * 16 + 4 * g + q;
+          const int row = (wr + RW * i) * 16 + 4 * g + q;
           if (row < ti.rows)
             H[static_cast<size_t>(ti.row0 + row) * a.m + f] =
                 f32_to_bf16(silu(acc[i][fl * 2][q]) * acc[i][fl * 2 + 1][q]);
@@ -307,7 +330,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       for (int i = 0; i < MW; ++i)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int row = (wr + 4 * i) * 16 + 4 * g + q;
+          const int row = (wr + RW * i) * 16 + 4 * g + q;
           if (row < ti.rows) {
             bf16_t *yr = Y + static_cast<size_t>(ti.row0 + row) * a.d + n;
             yr[0] = f32_to_bf16(acc[i][fl * 2][q]);
@@ -321,8 +344,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
 // tile width in features (gate/up) or output columns (down) for CG column groups
 template <bool GATEUP> constexpr int tile_width(int cg) { return GATEUP ? 16 * cg : 32 * cg; }
 
-template <bool GATEUP, int CG>
-__global__ __launch_bounds__(kWaves * 64) void grouped_gemm_bf16_kernel(GemmArgs a) {
+template <bool GATEUP, int CG, int W>
+__global__ __launch_bounds__(W * 64) void grouped_gemm_bf16_kernel(GemmArgs a) {
   const int nN = (GATEUP ? a.m : a.d) / tile_width<GATEUP>(CG);
   int grp, nt;
   map_block(blockIdx.x, nN, &grp, &nt);
@@ -331,13 +354,13 @@ __global__ __launch_bounds__(kWaves * 64) void grouped_gemm_bf16_kernel(GemmArgs
   __shared__ __align__(16) uint8_t smem[kLdsBytes];
   const int blocks = (ti.rows + 15) >> 4;
   if (blocks <= 4)
-    gemm_tile<GATEUP, 4, CG, stage_halves<CG>()>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 4, CG, stage_halves<CG>(), W>(a, ti, nt, smem);
   else if (blocks <= 8)
-    gemm_tile<GATEUP, 8, CG, stage_halves<CG>()>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 8, CG, stage_halves<CG>(), W>(a, ti, nt, smem);
   else if (blocks <= 12)
-    gemm_tile<GATEUP, 12, CG, stage_halves<CG>()>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 12, CG, stage_halves<CG>(), W>(a, ti, nt, smem);
   else
-    gemm_tile<GATEUP, 16, CG, stage_halves<CG>()>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 16, CG, stage_halves<CG>(), W>(a, ti, nt, smem);
 }
 
 // ------------------------------------------------------------------ fp32 (tiled FMA)
@@ -452,11 +475,11 @@ hipError_t launch_gateup(const GemmArgs &a, bool bf16, hipStream_t stream) {
   {
     // 128 features per tile when they divide m, else 64
     if (a.m % tile_width<true>(8) == 0)
-      grouped_gemm_bf16_kernel<true, 8>
-          <<<dim3(grid_for(a.max_groups, a.m / tile_width<true>(8))), kWaves * 64, 0, stream>>>(a);
+      grouped_gemm_bf16_kernel<true, 8, kGemmWaves>
+          <<<dim3(grid_for(a.max_groups, a.m / tile_width<true>(8))), kGemmWaves * 64, 0, stream>>>(a);
     else
-      grouped_gemm_bf16_kernel<true, 4>
-          <<<dim3(grid_for(a.max_groups, a.m / tile_width<true>(4))), kWaves * 64, 0, stream>>>(a);
+      grouped_gemm_bf16_kernel<true, 4, kGemmWaves>
+          <<<dim3(grid_for(a.max_groups, a.m / tile_width<true>(4))), kGemmWaves * 64, 0, stream>>>(a);
   }
   else
     gateup_f32_kernel<<<dim3(grid_for(a.max_groups, a.m / F_BN)), 256, 0, stream>>>(a);
@@ -469,11 +492,11 @@ hipError_t launch_down(const GemmArgs &a, bool bf16, hipStream_t stream) {
   {
     // 256 output columns per tile when they divide d, else 128
     if (a.d % tile_width<false>(8) == 0)
-      grouped_gemm_bf16_kernel<false, 8>
-          <<<dim3(grid_for(a.max_groups, a.d / tile_width<false>(8))), kWaves * 64, 0, stream>>>(a);
+      grouped_gemm_bf16_kernel<false, 8, kGemmWaves>
+          <<<dim3(grid_for(a.max_groups, a.d / tile_width<false>(8))), kGemmWaves * 64, 0, stream>>>(a);
     else
-      grouped_gemm_bf16_kernel<false, 4>
-          <<<dim3(grid_for(a.max_groups, a.d / tile_width<false>(4))), kWaves * 64, 0, stream>>>(a);
+      grouped_gemm_bf16_kernel<false, 4, kGemmWaves>
+          <<<dim3(grid_for(a.max_groups, a.d / tile_width<false>(4))), kGemmWaves * 64, 0, stream>>>(a);
   }
   else
     down_f32_kernel<<<dim3(grid_for(a.max_groups, a.d / F_BN)), 256, 0, stream>>>(a);
