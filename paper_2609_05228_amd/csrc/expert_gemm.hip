@@ -34,13 +34,13 @@
 // Launch order is XCD-aware: workgroups are dealt to the 8 XCDs round-robin, so
 // block b runs on XCD b % 8; the N tiles of one M tile are mapped to one XCD so
 // the activation rows they share stay in that XCD's L2.
-#include "ace_internal.h"
+#include "lds_dma.h"
 
 namespace ace {
 
 namespace {
 
-constexpr int kFragBytes = 1024;     // one MFMA fragment: 16 rows x 32 bf16
+constexpr int kFragBytes = kUnitBytes;  // one staged unit (8 rows x 64 bf16, or 16 rows x 32)
 constexpr int kLdsBytes = 160 * 1024;
 
 struct TileInfo {
@@ -73,52 +73,6 @@ __device__ __forceinline__ TileInfo tile_info(const GemmArgs &a, int grp) {
 
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }
 
-__device__ __forceinline__ uint32_t lds_addr(const void *p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void *)p));
-}
-
-// 16 bytes per lane from global `src` into LDS at lds_base + 16 * lane.  M0 is
-// saved and restored around the DMA so the compiler's use of it is unaffected.
-// The compiler does not see this LDS write: every consumer waits on vmcnt and
-// crosses a barrier explicitly.
-__device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
-  uint32_t saved;
-  asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_base))
-      : "memory");
-}
-
-__device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
-
-// wait until at most n (0..63) of this wave's vector memory operations are outstanding
-__device__ __forceinline__ void wait_vmcnt(int n) {
-#define ACE_VMCNT_CASE(c) \
-  case c:                 \
-    asm volatile("s_waitcnt vmcnt(" #c ")" ::: "memory"); \
-    break;
-  switch (n) {
-    ACE_VMCNT_CASE(0) ACE_VMCNT_CASE(1) ACE_VMCNT_CASE(2) ACE_VMCNT_CASE(3) ACE_VMCNT_CASE(4)
-    ACE_VMCNT_CASE(5) ACE_VMCNT_CASE(6) ACE_VMCNT_CASE(7) ACE_VMCNT_CASE(8) ACE_VMCNT_CASE(9)
-    ACE_VMCNT_CASE(10) ACE_VMCNT_CASE(11) ACE_VMCNT_CASE(12) ACE_VMCNT_CASE(13) ACE_VMCNT_CASE(14)
-    ACE_VMCNT_CASE(15) ACE_VMCNT_CASE(16) ACE_VMCNT_CASE(17) ACE_VMCNT_CASE(18) ACE_VMCNT_CASE(19)
-    ACE_VMCNT_CASE(20) ACE_VMCNT_CASE(21) ACE_VMCNT_CASE(22) ACE_VMCNT_CASE(23) ACE_VMCNT_CASE(24)
-    ACE_VMCNT_CASE(25) ACE_VMCNT_CASE(26) ACE_VMCNT_CASE(27) ACE_VMCNT_CASE(28) ACE_VMCNT_CASE(29)
-    ACE_VMCNT_CASE(30) ACE_VMCNT_CASE(31) ACE_VMCNT_CASE(32) ACE_VMCNT_CASE(33) ACE_VMCNT_CASE(34)
-    ACE_VMCNT_CASE(35) ACE_VMCNT_CASE(36) ACE_VMCNT_CASE(37) ACE_VMCNT_CASE(38) ACE_VMCNT_CASE(39)
-    ACE_VMCNT_CASE(40) ACE_VMCNT_CASE(41) ACE_VMCNT_CASE(42) ACE_VMCNT_CASE(43) ACE_VMCNT_CASE(44)
-    ACE_VMCNT_CASE(45) ACE_VMCNT_CASE(46) ACE_VMCNT_CASE(47) ACE_VMCNT_CASE(48) ACE_VMCNT_CASE(49)
-    ACE_VMCNT_CASE(50) ACE_VMCNT_CASE(51) ACE_VMCNT_CASE(52) ACE_VMCNT_CASE(53) ACE_VMCNT_CASE(54)
-    ACE_VMCNT_CASE(55) ACE_VMCNT_CASE(56) ACE_VMCNT_CASE(57) ACE_VMCNT_CASE(58) ACE_VMCNT_CASE(59)
-    ACE_VMCNT_CASE(60) ACE_VMCNT_CASE(61) ACE_VMCNT_CASE(62) ACE_VMCNT_CASE(63)
-    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-  }
-#undef ACE_VMCNT_CASE
-}
 
 constexpr int kGemmWaves = 8;  // waves per workgroup (two per SIMD)
 // 32-wide k halves per pipeline stage.  Two (64-wide stages) measured faster than
@@ -212,9 +166,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   const bf16_t *act = static_cast<const bf16_t *>(a.act);
   // A units this wave stages per stage (wave-uniform)
   const int na = P::FA > wave ? (P::FA - wave + W - 1) / W : 0;
-  // DMA lane -> (row in unit, source chunk): the lane lands in slot lane & 7 of row lane >> 3
-  const int ur = lane >> 3;
-  const int uc0 = (lane & 7) ^ ur;  // chunk for row half 0; half 1 flips bit 0
+  const int ur = lane >> 3;  // DMA lane -> row in its unit
 
   // A units this wave stages: u = wave + W j -> row block u / 2, row half u % 2 (= wave % 2)
   const bf16_t *asrc[NAM];
@@ -223,7 +175,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     const int u = min(wave + W * j, P::FA - 1);
     const int row = min((u >> 1) * 16 + (u & 1) * 8 + ur, ti.rows - 1);  // rows past the tile repeat its last row
     const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
-    asrc[j] = act + static_cast<size_t>(src_row) * K + 8 * (uc0 ^ (u & 1));
+    asrc[j] = act + static_cast<size_t>(src_row) * K + 8 * unit_chunk(lane, u & 1);
   }
   // B units this wave stages: b = wave * NB + t -> block b / 2, row half t % 2
   const bf16_t *bsrc[NB];
@@ -232,7 +184,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     const int b = wave * NB + t;
     const int blk = b >> 1, j = b & 1;
     const int fg = blk >> 1, cb = blk & 1;
-    const int c = 8 * (uc0 ^ j);
+    const int c = 8 * unit_chunk(lane, j);
     if (GATEUP) {
       const size_t f = static_cast<size_t>(ti.e) * a.m + nt * BN + fg * 16 + 8 * j + ur;
       bsrc[t] = static_cast<const bf16_t *>(cb ? a.w1 : a.w0) + f * a.d + c;
@@ -241,11 +193,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       bsrc[t] = static_cast<const bf16_t *>(a.w0) + n * a.m + c;
     }
   }
-  // fragment read offsets inside a 16-row block (two units) for k half h:
-  // row r16 sits in unit half r16 / 8, its chunk 4h + g in slot (4h + g) ^ (r16 % 8) ^ (r16 / 8)
-  const int rlo = r16 & 7, uh = r16 >> 3;
-  const int rd_off0 = uh * kFragBytes + rlo * 128 + ((g ^ rlo ^ uh) << 4);
-  const int rd_off1 = uh * kFragBytes + rlo * 128 + (((4 + g) ^ rlo ^ uh) << 4);
+  // fragment read offsets inside a 16-row block (two units) for k halves 0 and 1
+  const int rd_off0 = unit_read_offset(lane, 0), rd_off1 = unit_read_offset(lane, 1);
   const uint32_t ldsA = lds_addr(smem);
   const uint32_t ldsB = ldsA + SA * P::ASZ;
   const uint8_t *smemA = smem;

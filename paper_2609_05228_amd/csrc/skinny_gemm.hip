@@ -3,14 +3,17 @@
 // GEMVs.  Work is split so that thousands of waves stream weights at once:
 //  * a work item is one wave: one tile (expert) x 16 features (gate/up: a gate
 //    block and an up block) or 32 output columns (down) x one K split;
-//  * the wave loads its weight and activation MFMA fragments straight into
-//    registers through a P-stage ring (no LDS, no barriers) and multiplies them
-//    with v_mfma_f32_16x16x32_bf16;
+//  * the wave streams its weight rows and its activation rows into a private
+//    LDS ring with global_load_lds_dwordx4, one 8-row x 128-byte unit per
+//    instruction (whole cache lines; see lds_dma.h), P stages of 64 k deep, and
+//    waits only on its own vmcnt: no barriers, waves run independently;
+//  * it reads MFMA fragments back from the ring and multiplies them with
+//    v_mfma_f32_16x16x32_bf16;
 //  * with one K split the epilogue writes H (SwiGLU applied) or Y in bf16;
 //    with several, it writes fp32 partial sums, which swiglu_reduce_kernel (for
 //    H) and the combine kernel (for Y) add in split order, so the result does
 //    not depend on scheduling.
-#include "ace_internal.h"
+#include "lds_dma.h"
 
 namespace ace {
 
@@ -39,71 +42,67 @@ __device__ __forceinline__ TileInfo skinny_tile(const GemmArgs &a, int grp) {
 
 __device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }
 
-// ring depth: registers for P stages of 4 weight + 2*MB activation fragments
-template <int MB> struct Ring {
-  static constexpr int P = MB == 1 ? 8 : MB == 2 ? 6 : 4;
+constexpr int kSkinnyWavesPerGroup = 4;
+constexpr int kSkinnyRingBytes = 20 * 1024;  // LDS ring of one wave (4 waves: 80 KB, two workgroups per CU)
+
+// ring geometry for AU activation units per stage: a stage holds 4 weight units
+// (2 blocks x 2 row halves) then the activation units (2 per 16-row block, or
+// just one when the tile has at most 8 rows)
+template <int AU> struct SkinnyRing {
+  static constexpr int NU = 4 + AU;                                    // units (DMAs) per stage
+  static constexpr int STAGE = NU * kUnitBytes;
+  static constexpr int P = kSkinnyRingBytes / STAGE;                   // stages in the ring
+  static_assert(P >= 2, "ring too shallow");
+  static_assert((P - 1) * NU <= 63, "outstanding DMAs exceed the wait table");
 };
 
-template <int MB> struct Stage {
-  uint4 b[2][2];   // [block][k half]
-  uint4 a[MB][2];  // [row block][k half]
-};
+// whether a ring holds two stages of a 32-row (two-block) item
+constexpr bool kSkinnyTwoBlocks = kSkinnyRingBytes / ((4 + 4) * kUnitBytes) >= 2;
 
-template <int MB>
-__device__ __forceinline__ void load_stage(Stage<MB> &st, const bf16_t *const (&bsrc)[2],
-                                           const bf16_t *const (&asrc)[MB], int k) {
-#pragma unroll
-  for (int cb = 0; cb < 2; ++cb)
-#pragma unroll
-    for (int h = 0; h < 2; ++h) st.b[cb][h] = *reinterpret_cast<const uint4 *>(bsrc[cb] + k + 32 * h);
-#pragma unroll
-  for (int mi = 0; mi < MB; ++mi)
-#pragma unroll
-    for (int h = 0; h < 2; ++h) st.a[mi][h] = *reinterpret_cast<const uint4 *>(asrc[mi] + k + 32 * h);
-}
-
-template <int MB>
-__device__ __forceinline__ void mma_stage(const Stage<MB> &st, f32x4_t (&acc)[MB][2]) {
-#pragma unroll
-  for (int h = 0; h < 2; ++h)
-#pragma unroll
-    for (int mi = 0; mi < MB; ++mi)
-#pragma unroll
-      for (int cb = 0; cb < 2; ++cb)
-        acc[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, st.a[mi][h]),
-                                                              __builtin_bit_cast(bf16x8_t, st.b[cb][h]),
-                                                              acc[mi][cb], 0, 0, 0);
-}
-
-template <bool GATEUP, int MB>
-__device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo &ti, int nb, int s) {
-  constexpr int P = Ring<MB>::P;
+template <bool GATEUP, int MB, int AU>
+__device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo &ti, int nb, int s, uint8_t *ring) {
+  static_assert(AU == 2 * MB || (MB == 1 && AU == 1), "activation units cover the row blocks");
+  using R = SkinnyRing<AU>;
+  constexpr int P = R::P, NU = R::NU;
   const GemmArgs &a = sa.g;
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, g = lane >> 4;
+  const int ur = lane >> 3;  // DMA lane -> row in its unit
   const int K = GATEUP ? a.d : a.m;
   const int kc = K / sa.splits;
   const int kbase = s * kc;
   const int nk = kc / 64;
 
-  const bf16_t *bsrc[2];
-  if (GATEUP) {
-    const size_t f = static_cast<size_t>(ti.e) * a.m + nb * 16 + r16;
-    bsrc[0] = static_cast<const bf16_t *>(a.w0) + f * a.d + kbase + 8 * g;
-    bsrc[1] = static_cast<const bf16_t *>(a.w1) + f * a.d + kbase + 8 * g;
-  } else {
-    const size_t n = static_cast<size_t>(ti.e) * a.d + nb * 32 + r16;
-    bsrc[0] = static_cast<const bf16_t *>(a.w0) + n * a.m + kbase + 8 * g;
-    bsrc[1] = bsrc[0] + static_cast<size_t>(16) * a.m;
-  }
-  const bf16_t *act = static_cast<const bf16_t *>(a.act);
-  const bf16_t *asrc[MB];
+  // weight units t = 2 cb + j: block cb (gate/up: gate, up; down: 16-column halves), row half j
+  const bf16_t *src[NU];
 #pragma unroll
-  for (int mi = 0; mi < MB; ++mi) {
-    const int row = min(mi * 16 + r16, ti.rows - 1);  // rows past the tile repeat its last row
-    const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
-    asrc[mi] = act + static_cast<size_t>(src_row) * K + kbase + 8 * g;
+  for (int t = 0; t < 4; ++t) {
+    const int cb = t >> 1, j = t & 1;
+    const int c = kbase + 8 * unit_chunk(lane, j);
+    if (GATEUP) {
+      const size_t f = static_cast<size_t>(ti.e) * a.m + nb * 16 + 8 * j + ur;
+      src[t] = static_cast<const bf16_t *>(cb ? a.w1 : a.w0) + f * a.d + c;
+    } else {
+      const size_t n = static_cast<size_t>(ti.e) * a.d + nb * 32 + cb * 16 + 8 * j + ur;
+      src[t] = static_cast<const bf16_t *>(a.w0) + n * a.m + c;
+    }
   }
+  // activation units 4 + 2 mi + j: row block mi, row half j (AU == 1: rows 0-7 only)
+  const bf16_t *act = static_cast<const bf16_t *>(a.act);
+#pragma unroll
+  for (int t = 4; t < NU; ++t) {
+    const int mi = (t - 4) >> 1, j = t & 1;
+    const int row = min(mi * 16 + 8 * j + ur, ti.rows - 1);  // rows past the tile repeat its last row
+    const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
+    src[t] = act + static_cast<size_t>(src_row) * K + kbase + 8 * unit_chunk(lane, j);
+  }
+  const uint32_t ring_lds = lds_addr(ring);
+  // stage st -> slot st % P; its units at slot * STAGE + t * kUnitBytes
+  auto issue = [&](int st) {
+    const uint32_t base = ring_lds + (st % P) * R::STAGE;
+#pragma unroll
+    for (int t = 0; t < NU; ++t) dma16(src[t] + st * 64, base + t * kUnitBytes);
+  };
 
   f32x4_t acc[MB][2];
 #pragma unroll
@@ -111,17 +110,32 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
     acc[mi][0] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     acc[mi][1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
-  Stage<MB> ring[P];
+  const int rd0 = unit_read_offset(lane, 0), rd1 = unit_read_offset(lane, 1);
+  // with one activation unit, lanes of rows 8-15 (past the tile) read inside that unit
+  const int ra0 = (AU == 1 && (lane & 8)) ? rd0 - kUnitBytes : rd0;
+  const int ra1 = (AU == 1 && (lane & 8)) ? rd1 - kUnitBytes : rd1;
+  for (int st = 0; st < P - 1 && st < nk; ++st) issue(st);
+  for (int kt = 0; kt < nk; ++kt) {
+    if (kt + P - 1 < nk) {
+      // the slot it refills held stage kt-1, whose LDS reads this wave issued last iteration
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      issue(kt + P - 1);
+    }
+    wait_vmcnt(NU * min(P - 1, nk - 1 - kt));  // stage kt landed
+    const uint8_t *sl = ring + (kt % P) * R::STAGE;
 #pragma unroll
-  for (int u = 0; u < P; ++u)
-    if (u < nk) load_stage<MB>(ring[u], bsrc, asrc, u * 64);
-  for (int k0 = 0; k0 < nk; k0 += P) {
+    for (int h = 0; h < 2; ++h) {
+      const int rd = h ? rd1 : rd0, ra = h ? ra1 : ra0;
+      bf16x8_t bf[2];
 #pragma unroll
-    for (int u = 0; u < P; ++u) {
-      const int kt = k0 + u;
-      if (kt < nk) {
-        mma_stage<MB>(ring[u], acc);
-        if (kt + P < nk) load_stage<MB>(ring[u], bsrc, asrc, (kt + P) * 64);
+      for (int cb = 0; cb < 2; ++cb)
+        bf[cb] = *reinterpret_cast<const bf16x8_t *>(sl + cb * 2 * kUnitBytes + rd);
+#pragma unroll
+      for (int mi = 0; mi < MB; ++mi) {
+        const bf16x8_t av = *reinterpret_cast<const bf16x8_t *>(sl + (4 + 2 * mi) * kUnitBytes + ra);
+#pragma unroll
+        for (int cb = 0; cb < 2; ++cb)
+          acc[mi][cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bf[cb], acc[mi][cb], 0, 0, 0);
       }
     }
   }
@@ -160,10 +174,13 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
 
 // one wave per work item; item = ((grp * splits) + s) * nN + nb
 template <bool GATEUP>
-__global__ __launch_bounds__(256) void skinny_gemm_kernel(SkinnyArgs sa) {
+__global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(SkinnyArgs sa) {
+  __shared__ __align__(16) uint8_t smem[kSkinnyWavesPerGroup * kSkinnyRingBytes];
   const GemmArgs &a = sa.g;
   const int nN = GATEUP ? a.m / 16 : a.d / 32;
-  const long item = static_cast<long>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  const int wave = threadIdx.x >> 6;
+  uint8_t *ring = smem + wave * kSkinnyRingBytes;
+  const long item = static_cast<long>(blockIdx.x) * kSkinnyWavesPerGroup + wave;
   const int nb = static_cast<int>(item % nN);
   const long rest = item / nN;
   const int s = static_cast<int>(rest % sa.splits);
@@ -172,12 +189,25 @@ __global__ __launch_bounds__(256) void skinny_gemm_kernel(SkinnyArgs sa) {
   const TileInfo ti = skinny_tile(a, grp);
   if (!ti.valid) return;
   const int blocks = (ti.rows + 15) >> 4;
-  if (blocks <= 1)
-    skinny_item<GATEUP, 1>(sa, ti, nb, s);
-  else if (blocks <= 2)
-    skinny_item<GATEUP, 2>(sa, ti, nb, s);
-  else
-    skinny_item<GATEUP, 4>(sa, ti, nb, s);
+  if (ti.rows <= 8) {
+    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, ring);
+  } else if (blocks <= 1 || !kSkinnyTwoBlocks) {
+    // 16 rows per pass (more than 16 rows re-read the weights, mostly from L2)
+    for (int r = 0; r < ti.rows; r += 16) {
+      TileInfo part = ti;
+      part.row0 = ti.row0 + r;
+      part.rows = min(16, ti.rows - r);
+      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, ring);
+    }
+  } else if constexpr (kSkinnyTwoBlocks) {
+    // 32 rows per pass
+    for (int r = 0; r < ti.rows; r += 32) {
+      TileInfo part = ti;
+      part.row0 = ti.row0 + r;
+      part.rows = min(32, ti.rows - r);
+      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, ring);
+    }
+  }
 }
 
 // H = SiLU(sum_s gate partials) * (sum_s up partials), splits added in order
@@ -205,9 +235,9 @@ hipError_t launch_skinny(const SkinnyArgs &sa, bool gateup, const int32_t *n_row
   if (a.max_groups <= 0) return hipSuccess;
   const long nN = gateup ? a.m / 16 : a.d / 32;
   const long items = static_cast<long>(a.max_groups) * sa.splits * nN;
-  const dim3 grid(static_cast<unsigned>((items + 3) / 4));
+  const dim3 grid(static_cast<unsigned>((items + kSkinnyWavesPerGroup - 1) / kSkinnyWavesPerGroup));
   if (gateup) {
-    skinny_gemm_kernel<true><<<grid, 256, 0, stream>>>(sa);
+    skinny_gemm_kernel<true><<<grid, kSkinnyWavesPerGroup * 64, 0, stream>>>(sa);
     if (sa.splits > 1) {
       const size_t total = static_cast<size_t>(sa.rows_cap) * a.m;
       size_t blocks = (total + 255) / 256;
@@ -215,7 +245,7 @@ hipError_t launch_skinny(const SkinnyArgs &sa, bool gateup, const int32_t *n_row
       swiglu_reduce_kernel<<<dim3(static_cast<unsigned>(blocks)), 256, 0, stream>>>(sa, n_rows);
     }
   } else {
-    skinny_gemm_kernel<false><<<grid, 256, 0, stream>>>(sa);
+    skinny_gemm_kernel<false><<<grid, kSkinnyWavesPerGroup * 64, 0, stream>>>(sa);
   }
   return hipGetLastError();
 }
