@@ -172,10 +172,24 @@ __device__ __forceinline__ void load_stage(Stage<T, NT> &st, const T *xrow, cons
 
 // live = false: the stage holds a clamped (already counted) block; its
 // activations are taken as zero so the MFMAs need no branch
+// bf16 fragments arrive row-major: lane l holds 16 bytes (l % 4) of the 64 of
+// row l / 4, so four consecutive lanes read one contiguous 64-byte run (MFMA
+// operand order, lane l -> row l % 16, spreads every 16 lanes over 16 rows and
+// streams about 3x slower from L2).  ds_bpermute moves them to operand order:
+// lane l takes the data of lane 4 (l % 16) + l / 16.
+__device__ __forceinline__ uint4 to_operand_order(const uint4 v) {
+  const int lane = threadIdx.x & 63;
+  const int src = (4 * (lane & 15) + (lane >> 4)) << 2;
+  return make_uint4(static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src, static_cast<int>(v.x))),
+                    static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src, static_cast<int>(v.y))),
+                    static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src, static_cast<int>(v.z))),
+                    static_cast<uint32_t>(__builtin_amdgcn_ds_bpermute(src, static_cast<int>(v.w))));
+}
+
 template <int NT>
 __device__ __forceinline__ void mma_stage(const Stage<bf16_t, NT> &st, f32x4_t (&acc)[NT], float &ss, bool live) {
   float xv[8], gv[8];
-  const uint4 xr = live ? st.x : make_uint4(0u, 0u, 0u, 0u);
+  const uint4 xr = live ? to_operand_order(st.x) : make_uint4(0u, 0u, 0u, 0u);
   Oct<bf16_t>::cvt(xr, xv);
   Oct<bf16_t>::cvt(st.g, gv);
   uint32_t hi[4], lo[4];
@@ -196,12 +210,13 @@ __device__ __forceinline__ void mma_stage(const Stage<bf16_t, NT> &st, f32x4_t (
   }
   const bf16x8_t ahi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
   const bf16x8_t alo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+  bf16x8_t w[NT];
 #pragma unroll
-  for (int f = 0; f < NT; ++f)
-    acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, __builtin_bit_cast(bf16x8_t, st.w[f]), acc[f], 0, 0, 0);
+  for (int f = 0; f < NT; ++f) w[f] = __builtin_bit_cast(bf16x8_t, to_operand_order(st.w[f]));
 #pragma unroll
-  for (int f = 0; f < NT; ++f)
-    acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, __builtin_bit_cast(bf16x8_t, st.w[f]), acc[f], 0, 0, 0);
+  for (int f = 0; f < NT; ++f) acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, w[f], acc[f], 0, 0, 0);
+#pragma unroll
+  for (int f = 0; f < NT; ++f) acc[f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, w[f], acc[f], 0, 0, 0);
 }
 
 template <int NT>
@@ -232,44 +247,59 @@ template <typename T, int NT> struct Depth {
   static constexpr int value = fit >= 4 ? 4 : fit >= 1 ? fit : 1;
 };
 
-// Blocks j = jfirst, jfirst + step, ... < jend of one wave: each round loads D
-// blocks, then multiplies them; indexes past jend are clamped (their data is
-// zeroed in the multiply), so every load is unconditional.
+// Blocks jfirst + step i (i < cnt, cnt = blocks below jend) of one wave, in
+// the order i = rot, rot + 1, ... (mod cnt): workgroups that start together
+// use different rotations so they do not all request the same router rows at
+// once.  Each round loads D blocks, then multiplies them; rounds past the end
+// load the last block again and zero its activations in the multiply, so
+// every load is unconditional.
 template <typename T, int NT>
 __device__ __forceinline__ void accumulate_logits(const T *xrow, const T *gl, const T *wl, const int (&woff)[NT],
-                                                  int jfirst, int jend, int step, f32x4_t (&acc)[NT], float &ss) {
+                                                  int jfirst, int jend, int step, int rot, f32x4_t (&acc)[NT],
+                                                  float &ss) {
   constexpr int D = Depth<T, NT>::value;
-  const int last = jend - 1;
-  for (int j = jfirst; j < jend; j += D * step) {
+  const int cnt = jend > jfirst ? (jend - jfirst + step - 1) / step : 0;
+  if (cnt == 0) return;
+  rot %= cnt;
+  for (int i0 = 0; i0 < cnt; i0 += D) {
     Stage<T, NT> st[D];
 #pragma unroll
-    for (int u = 0; u < D; ++u) load_stage<T, NT>(st[u], xrow, gl, wl, woff, 32 * min(j + u * step, last));
+    for (int u = 0; u < D; ++u) {
+      int i = min(i0 + u, cnt - 1) + rot;
+      i = i >= cnt ? i - cnt : i;
+      load_stage<T, NT>(st[u], xrow, gl, wl, woff, 32 * (jfirst + i * step));
+    }
 #pragma unroll
-    for (int u = 0; u < D; ++u) mma_stage<NT>(st[u], acc, ss, j + u * step < jend);
+    for (int u = 0; u < D; ++u) mma_stage<NT>(st[u], acc, ss, i0 + u < cnt);
   }
 }
 
 // One wave's partial logits of blocks jfirst, jfirst + step, ... < jend for
 // the 16 tokens from t0, into zred[token][expert] and ssred[token] (LDS).
 template <typename T, int NT, int ZS>
-__device__ __forceinline__ void wave_logits(const RouteArgs &a, int t0, int jfirst, int jend, int step,
+__device__ __forceinline__ void wave_logits(const RouteArgs &a, int t0, int jfirst, int jend, int step, int rot,
                                             float (*zred)[ZS], float *ssred) {
   const T *x = static_cast<const T *>(a.x);
   const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, grp = lane >> 4;
   const int d = a.d, N = a.N;
-  const int trow = min(t0 + r16, a.T - 1);  // rows past the batch repeat the last token
-  const T *xrow = x + static_cast<size_t>(trow) * d + grp * 8;
+  // row and 8-element chunk this lane loads: bf16 rows are loaded row-major
+  // (row lane / 4, chunk lane % 4) and permuted into operand order in
+  // mma_stage; fp32 rows are loaded in operand order (row lane % 16, chunk lane / 16)
+  constexpr bool kRowMajor = sizeof(T) == 2;
+  const int lrow = kRowMajor ? lane >> 2 : r16, lchunk = kRowMajor ? lane & 3 : grp;
+  const int trow = min(t0 + lrow, a.T - 1);  // rows past the batch repeat the last token
+  const T *xrow = x + static_cast<size_t>(trow) * d + lchunk * 8;
   const T *gl = static_cast<const T *>(a.gamma) + grp * 8;
-  const T *wl = static_cast<const T *>(a.w_router) + grp * 8;
+  const T *wl = static_cast<const T *>(a.w_router) + lchunk * 8;
   int woff[NT];
 #pragma unroll
-  for (int f = 0; f < NT; ++f) woff[f] = min(16 * f + r16, N - 1) * d;
+  for (int f = 0; f < NT; ++f) woff[f] = min(16 * f + lrow, N - 1) * d;
   f32x4_t acc[NT];
 #pragma unroll
   for (int f = 0; f < NT; ++f) acc[f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float ss = 0.f;
-  accumulate_logits<T, NT>(xrow, gl, wl, woff, jfirst, jend, step, acc, ss);
+  accumulate_logits<T, NT>(xrow, gl, wl, woff, jfirst, jend, step, rot, acc, ss);
   // D[row = token 4 grp + i][col = expert 16 f + r16]
 #pragma unroll
   for (int f = 0; f < NT; ++f)
@@ -297,7 +327,7 @@ __global__ __launch_bounds__(256) void route_partial_kernel(RouteArgs a) {
   const int s = blockIdx.y;
   const int nbs = (a.d >> 5) / a.ksplit;  // blocks per slice
   if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) a.ticket[0] = 0u;  // for the select kernel's plan
-  wave_logits<T, NT, NP + 1>(a, t0, s * nbs + wave, (s + 1) * nbs, kPartWaves, zred[wave], ssred[wave]);
+  wave_logits<T, NT, NP + 1>(a, t0, s * nbs + wave, (s + 1) * nbs, kPartWaves, blockIdx.x, zred[wave], ssred[wave]);
   __syncthreads();
   const size_t plane = static_cast<size_t>(s) * a.T;
   for (int idx = tid; idx < kTok * NP; idx += 256) {
@@ -465,7 +495,8 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
     __syncthreads();
   } else {
     // ---- 1. logits over all K: wave w takes blocks w, w + 8, ...
-    wave_logits<T, NT, NP + 1>(a, t0, wave, d >> 5, kWaves, zred[wave], ssred[wave]);
+    // workgroups are dealt to the 8 XCDs round-robin: rotate by the index on the XCD
+    wave_logits<T, NT, NP + 1>(a, t0, wave, d >> 5, kWaves, blockIdx.x >> 3, zred[wave], ssred[wave]);
     __syncthreads();
     if (tid < kTok) {
       float ssum = 0.f;
