@@ -368,10 +368,14 @@ __device__ __forceinline__ void plan_if_last(const RouteArgs &a) {
   if (!last) return;
   __threadfence();
   for (int e = tid; e < N; e += 512) {
+    int c[kRouteMaxSplitChunks];
+#pragma unroll
+    for (int g = 0; g < kRouteMaxSplitChunks; ++g) c[g] = g < G ? a.chunk_count[static_cast<size_t>(g) * N + e] : 0;
     int run = 0;
-    for (int g = 0; g < G; ++g) {
-      base[g][e] = run;
-      run += a.chunk_count[static_cast<size_t>(g) * N + e];
+#pragma unroll
+    for (int g = 0; g < kRouteMaxSplitChunks; ++g) {
+      if (g < G) base[g][e] = run;
+      run += c[g];
     }
     cnt[e] = run;
     tcnt[e] = (run + kTileM - 1) / kTileM;
@@ -427,10 +431,12 @@ __device__ __forceinline__ void plan_if_last(const RouteArgs &a) {
   }
   const int slots = a.T * a.k;
   for (int o = tid; o < slots; o += 512) {
-    if (!a.keep[o]) continue;
-    const int t = o / a.k;
+    const bool kept = a.keep[o] != 0;
     const int e = a.topk_idx[o];
-    const int row = off[e] + base[t / kTok][e] + a.local_rank[o];
+    const int rank = a.local_rank[o];
+    if (!kept) continue;
+    const int t = o / a.k;
+    const int row = off[e] + base[t / kTok][e] + rank;
     a.perm[row] = t;
     a.slot_row[o] = row;
   }
@@ -467,24 +473,40 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   const float bias = (a.b_router && (tid % NP) < N) ? a.b_router[tid % NP] : 0.f;
 
   if constexpr (SPLIT) {
-    // ---- 1. add the K slices' partial logits and sums of squares in slice order
-    if (tid < kTok) {
-      float ssum = 0.f;
-      for (int sl = 0; sl < a.ksplit; ++sl) ssum += a.sspart[static_cast<size_t>(sl) * nt + min(t0 + tid, nt - 1)];
-      rstd_s[tid] = 1.0f / sqrtf(ssum / static_cast<float>(d) + a.rms_eps);
-    }
-    for (int idx = tid; idx < kTok * NP; idx += 512) {
+    // ---- 1. add the K slices' partial logits and sums of squares in slice
+    // order; every load of the workgroup is issued before the first add
+    constexpr int PER = (kTok * NP + 511) / 512;  // logits per thread
+    float ssp[kRouteMaxSlices];
+#pragma unroll
+    for (int sl = 0; sl < kRouteMaxSlices; ++sl)
+      ssp[sl] = (tid < kTok && sl < a.ksplit) ? a.sspart[static_cast<size_t>(sl) * nt + min(t0 + tid, nt - 1)] : 0.f;
+    float part[PER][kRouteMaxSlices];
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int idx = min(tid + 512 * u, kTok * NP - 1);
       const int tl = idx / NP;
       const int e = idx - tl * NP;
       const size_t col = static_cast<size_t>(min(t0 + tl, nt - 1)) * a.zstride + e;
-      float part[kRouteMaxSlices];
 #pragma unroll
       for (int sl = 0; sl < kRouteMaxSlices; ++sl)
-        part[sl] = sl < a.ksplit ? a.zpart[static_cast<size_t>(sl) * nt * a.zstride + col] : 0.f;
-      float z = 0.f;
+        part[u][sl] = sl < a.ksplit ? a.zpart[static_cast<size_t>(sl) * nt * a.zstride + col] : 0.f;
+    }
+    if (tid < kTok) {
+      float ssum = 0.f;
 #pragma unroll
-      for (int sl = 0; sl < kRouteMaxSlices; ++sl) z += part[sl];
-      zred[0][tl][e] = z;
+      for (int sl = 0; sl < kRouteMaxSlices; ++sl) ssum += ssp[sl];
+      rstd_s[tid] = 1.0f / sqrtf(ssum / static_cast<float>(d) + a.rms_eps);
+    }
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int idx = tid + 512 * u;
+      if (idx < kTok * NP) {
+        const int tl = idx / NP;
+        float z = 0.f;
+#pragma unroll
+        for (int sl = 0; sl < kRouteMaxSlices; ++sl) z += part[u][sl];
+        zred[0][tl][idx - tl * NP] = z;
+      }
     }
     __syncthreads();
     for (int idx = tid; idx < kTok * NP; idx += 512) {
