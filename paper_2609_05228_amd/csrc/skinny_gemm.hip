@@ -60,7 +60,8 @@ template <int AU> struct SkinnyRing {
 constexpr bool kSkinnyTwoBlocks = kSkinnyRingBytes / ((4 + 4) * kUnitBytes) >= 2;
 
 template <bool GATEUP, int MB, int AU>
-__device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo &ti, int nb, int s, uint8_t *ring) {
+__device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo &ti, int nb, int s, int rot,
+                                            uint8_t *ring) {
   static_assert(AU == 2 * MB || (MB == 1 && AU == 1), "activation units cover the row blocks");
   using R = SkinnyRing<AU>;
   constexpr int P = R::P, NU = R::NU;
@@ -97,11 +98,16 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
     src[t] = act + static_cast<size_t>(src_row) * K + kbase + 8 * unit_chunk(lane, j);
   }
   const uint32_t ring_lds = lds_addr(ring);
+  // Stage st covers the 64-wide K block (st + k0) % nk of this split: waves start
+  // at different K blocks, so rows 4 KB apart are not all read at one offset at
+  // once (that concentrates the stream on a few HBM channels).
+  const int k0 = rot % nk;
   // stage st -> slot st % P; its units at slot * STAGE + t * kUnitBytes
   auto issue = [&](int st) {
     const uint32_t base = ring_lds + (st % P) * R::STAGE;
+    const int kb = st + k0 < nk ? st + k0 : st + k0 - nk;
 #pragma unroll
-    for (int t = 0; t < NU; ++t) dma16(src[t] + st * 64, base + t * kUnitBytes);
+    for (int t = 0; t < NU; ++t) dma16(src[t] + kb * 64, base + t * kUnitBytes);
   };
 
   f32x4_t acc[MB][2];
@@ -189,15 +195,16 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
   const TileInfo ti = skinny_tile(a, grp);
   if (!ti.valid) return;
   const int blocks = (ti.rows + 15) >> 4;
+  const int rot = static_cast<int>(item & 0x7fffffff);
   if (ti.rows <= 8) {
-    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, ring);
+    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, rot, ring);
   } else if (blocks <= 1 || !kSkinnyTwoBlocks) {
     // 16 rows per pass (more than 16 rows re-read the weights, mostly from L2)
     for (int r = 0; r < ti.rows; r += 16) {
       TileInfo part = ti;
       part.row0 = ti.row0 + r;
       part.rows = min(16, ti.rows - r);
-      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, ring);
+      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, rot, ring);
     }
   } else if constexpr (kSkinnyTwoBlocks) {
     // 32 rows per pass
@@ -205,7 +212,7 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
       TileInfo part = ti;
       part.row0 = ti.row0 + r;
       part.rows = min(32, ti.rows - r);
-      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, ring);
+      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, rot, ring);
     }
   }
 }
