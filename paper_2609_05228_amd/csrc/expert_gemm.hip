@@ -207,17 +207,22 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     for (int c = 0; c < 2 * CW; ++c) acc[i][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nk = K / BK;
+  // Pipeline stage s covers K block (s + k0) % nk.  Workgroups start at different
+  // K blocks: rows 4 KB apart (d = 2048 bf16) read at one K offset by every
+  // workgroup at once concentrate on a few HBM channels and stream ~20% slower.
+  const int k0 = blockIdx.x % nk;
+  auto kofs = [&](int s) { return (s + k0 < nk ? s + k0 : s + k0 - nk) * BK; };
   // prologue: B stages 0..SB-2, then A stages 0..SA-2
   for (int s = 0; s < SB - 1 && s < nk; ++s) {
     const uint32_t st = ldsB + s * P::BSZ;
 #pragma unroll
-    for (int t = 0; t < NB; ++t) dma16(bsrc[t] + s * BK, st + (wave * NB + t) * kFragBytes);
+    for (int t = 0; t < NB; ++t) dma16(bsrc[t] + kofs(s), st + (wave * NB + t) * kFragBytes);
   }
   for (int s = 0; s < SA - 1 && s < nk; ++s) {
     const uint32_t st = ldsA + s * P::ASZ;
 #pragma unroll
     for (int j = 0; j < NAM; ++j)
-      if (j < na) dma16(asrc[j] + s * BK, st + (wave + W * j) * kFragBytes);
+      if (j < na) dma16(asrc[j] + kofs(s), st + (wave + W * j) * kFragBytes);
   }
 
   for (int kt = 0; kt < nk; ++kt) {
@@ -228,13 +233,13 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       const uint32_t st = ldsA + (s % SA) * P::ASZ;
 #pragma unroll
       for (int j = 0; j < NAM; ++j)
-        if (j < na) dma16(asrc[j] + s * BK, st + (wave + W * j) * kFragBytes);
+        if (j < na) dma16(asrc[j] + kofs(s), st + (wave + W * j) * kFragBytes);
     }
     if (kt + SB - 1 < nk) {
       const int s = kt + SB - 1;
       const uint32_t st = ldsB + (s % SB) * P::BSZ;
 #pragma unroll
-      for (int t = 0; t < NB; ++t) dma16(bsrc[t] + s * BK, st + (wave * NB + t) * kFragBytes);
+      for (int t = 0; t < NB; ++t) dma16(bsrc[t] + kofs(s), st + (wave * NB + t) * kFragBytes);
     }
     const uint8_t *sa = smemA + (kt % SA) * P::ASZ;
     const uint8_t *sb = smemB + (kt % SB) * P::BSZ;
