@@ -149,7 +149,7 @@ __device__ __forceinline__ int pending_ok(int kt, int nk, int na) {
 // banks.  Wave w computes row blocks wr, wr+RW, ... (wr = w/2) against the CG/2
 // column groups starting at wc*CG/2 (wc = w%2).
 template <bool GATEUP, int MB, int CG, int KH, int W>
-__device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, uint8_t *smem) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, int mrot, uint8_t *smem) {
   static_assert(KH == 2, "8-row DMA units span a 64-wide K stage");
   using P = Pipe<MB, CG, KH, W>;
   constexpr int RW = W / 2;    // waves along the rows
@@ -207,10 +207,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     for (int c = 0; c < 2 * CW; ++c) acc[i][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nk = K / BK;
-  // Pipeline stage s covers K block (s + k0) % nk.  Workgroups start at different
-  // K blocks: rows 4 KB apart (d = 2048 bf16) read at one K offset by every
-  // workgroup at once concentrate on a few HBM channels and stream ~20% slower.
-  const int k0 = blockIdx.x % nk;
+  // Pipeline stage s covers K block (s + k0) % nk, k0 set by the M tile.  M tiles
+  // start at different K blocks: rows 4 KB apart (d = 2048 bf16) read at one K
+  // offset by every workgroup at once concentrate on a few HBM channels and
+  // stream ~20% slower.  The N tiles of one M tile keep one K order, so the
+  // activation rows they all read are shared in their XCD's L2.
+  const int k0 = mrot % nk;
   auto kofs = [&](int s) { return (s + k0 < nk ? s + k0 : s + k0 - nk) * BK; };
   // prologue: B stages 0..SB-2, then A stages 0..SA-2
   for (int s = 0; s < SB - 1 && s < nk; ++s) {
@@ -308,13 +310,13 @@ __global__ __launch_bounds__(W * 64) void grouped_gemm_bf16_kernel(GemmArgs a) {
   __shared__ __align__(16) uint8_t smem[kLdsBytes];
   const int blocks = (ti.rows + 15) >> 4;
   if (blocks <= 4)
-    gemm_tile<GATEUP, 4, CG, stage_halves<CG>(), W>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 4, CG, stage_halves<CG>(), W>(a, ti, nt, grp, smem);
   else if (blocks <= 8)
-    gemm_tile<GATEUP, 8, CG, stage_halves<CG>(), W>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 8, CG, stage_halves<CG>(), W>(a, ti, nt, grp, smem);
   else if (blocks <= 12)
-    gemm_tile<GATEUP, 12, CG, stage_halves<CG>(), W>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 12, CG, stage_halves<CG>(), W>(a, ti, nt, grp, smem);
   else
-    gemm_tile<GATEUP, 16, CG, stage_halves<CG>(), W>(a, ti, nt, smem);
+    gemm_tile<GATEUP, 16, CG, stage_halves<CG>(), W>(a, ti, nt, grp, smem);
 }
 
 // ------------------------------------------------------------------ fp32 (tiled FMA)
