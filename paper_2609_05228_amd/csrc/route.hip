@@ -442,6 +442,64 @@ __device__ __forceinline__ void plan_if_last(const RouteArgs &a) {
   }
 }
 
+// One chunk (at most 16 tokens): its only select workgroup writes the plan
+// straight from the per-expert token masks in LDS and each kept slot's rank
+// (held by the slot's own lane), with no fence, ticket or global re-read.  Same
+// rows as plan_if_last: row = offsets[e] + rank.
+__device__ __forceinline__ void plan_one_chunk(const RouteArgs &a, const uint32_t *emask, bool kept, int e_mine,
+                                               int t, int sub, int rank) {
+  __shared__ int off1[kMaxN + 1];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int N = a.N;
+  if (tid < 64) {
+    // exclusive scans of the counts and tile counts (N <= 256: four per lane)
+    int s = 0, st = 0, loc[4], loct[4], c[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = lane * 4 + j;
+      c[j] = e < N ? __popc(emask[e]) : 0;
+      loc[j] = s;
+      loct[j] = st;
+      s += c[j];
+      st += (c[j] + kTileM - 1) / kTileM;
+    }
+    int inc = s, inct = st;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int v = __shfl_up(inc, o), vt = __shfl_up(inct, o);
+      if (lane >= o) {
+        inc += v;
+        inct += vt;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = lane * 4 + j;
+      if (e < N) {
+        const int off = inc - s + loc[j], toff = inct - st + loct[j];
+        off1[e] = off;
+        a.counts[e] = c[j];
+        a.offsets[e] = off;
+        for (int q = 0; q * kTileM < c[j]; ++q) {
+          a.tile_expert[toff + q] = e;
+          a.tile_row0[toff + q] = off + q * kTileM;
+          a.tile_rows[toff + q] = min(kTileM, c[j] - q * kTileM);
+        }
+      }
+    }
+    if (lane == 63) {
+      a.offsets[N] = inc;
+      a.n_tiles[0] = inct;
+    }
+  }
+  __syncthreads();
+  if (kept) {
+    const int row = off1[e_mine] + rank;
+    a.perm[row] = t;
+    a.slot_row[static_cast<size_t>(t) * a.k + sub] = row;
+  }
+}
+
 // NT = number of 16-expert tiles covered (N <= 16 * NT).  SPLIT: the logits
 // come from route_partial_kernel's K slices; otherwise the 8 waves compute
 // them here over all of K.
@@ -649,10 +707,14 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   // ---- per-expert token masks of this chunk -> local ranks and counts
   if (my_kept) atomicOr(&emask[my_e], 1u << tl);
   __syncthreads();
-  if (my_kept) {
-    const uint32_t below = emask[my_e] & ((1u << tl) - 1u);
-    a.local_rank[static_cast<size_t>(t) * a.k + sub] = static_cast<uint8_t>(__popc(below));
+  const int my_rank = my_kept ? __popc(emask[my_e] & ((1u << tl) - 1u)) : 0;
+  if constexpr (SPLIT) {
+    if (gridDim.x == 1) {
+      plan_one_chunk(a, emask, my_kept, my_e, t, sub, my_rank);
+      return;
+    }
   }
+  if (my_kept) a.local_rank[static_cast<size_t>(t) * a.k + sub] = static_cast<uint8_t>(my_rank);
   for (int e = tid; e < N; e += 512)
     a.chunk_count[static_cast<size_t>(blockIdx.x) * N + e] = static_cast<uint8_t>(__popc(emask[e]));
   if constexpr (SPLIT) plan_if_last(a);
