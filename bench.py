@@ -15,7 +15,7 @@ kernels, decode batches 1/8/32/64 (tau transferred from prefill), per-stage
 times from HIP events recorded on the layer's stream, the roofline of the
 dominant kernel and the CPU oracle timed on a bounded token sample.
 
-    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--prefill-only] [--no-cpu]
+    python bench.py [--gpus 1] [--steps 100] [--warmup 20] [--prefill-only] [--no-cpu]
 """
 from __future__ import annotations
 
@@ -56,8 +56,8 @@ def source_digest(src: str) -> str:
 def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--q", default="0.5", help="skip ratio whose stored tau is used")
     ap.add_argument("--prefill-only", action="store_true", help="time only the ACE prefill step")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")

@@ -533,21 +533,22 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   if constexpr (SPLIT) {
     // ---- 1. add the K slices' partial logits and sums of squares in slice
     // order; every load of the workgroup is issued before the first add
-    constexpr int PER = (kTok * NP + 511) / 512;  // logits per thread
+    constexpr int PER = (kTok * NP + 2047) / 2048;  // groups of 4 logits per thread (16-byte loads)
     float ssp[kRouteMaxSlices];
 #pragma unroll
     for (int sl = 0; sl < kRouteMaxSlices; ++sl)
       ssp[sl] = (tid < kTok && sl < a.ksplit) ? a.sspart[static_cast<size_t>(sl) * nt + min(t0 + tid, nt - 1)] : 0.f;
-    float part[PER][kRouteMaxSlices];
+    float4 part[PER][kRouteMaxSlices];
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      const int idx = min(tid + 512 * u, kTok * NP - 1);
+      const int idx = min(4 * tid + 2048 * u, kTok * NP - 4);
       const int tl = idx / NP;
       const int e = idx - tl * NP;
       const size_t col = static_cast<size_t>(min(t0 + tl, nt - 1)) * a.zstride + e;
 #pragma unroll
       for (int sl = 0; sl < kRouteMaxSlices; ++sl)
-        part[u][sl] = sl < a.ksplit ? a.zpart[static_cast<size_t>(sl) * nt * a.zstride + col] : 0.f;
+        part[u][sl] = sl < a.ksplit ? *reinterpret_cast<const float4 *>(a.zpart + static_cast<size_t>(sl) * nt * a.zstride + col)
+                                    : make_float4(0.f, 0.f, 0.f, 0.f);
     }
     if (tid < kTok) {
       float ssum = 0.f;
@@ -557,13 +558,22 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
     }
 #pragma unroll
     for (int u = 0; u < PER; ++u) {
-      const int idx = tid + 512 * u;
+      const int idx = 4 * tid + 2048 * u;
       if (idx < kTok * NP) {
         const int tl = idx / NP;
-        float z = 0.f;
+        float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-        for (int sl = 0; sl < kRouteMaxSlices; ++sl) z += part[u][sl];
-        zred[0][tl][idx - tl * NP] = z;
+        for (int sl = 0; sl < kRouteMaxSlices; ++sl) {
+          z.x += part[u][sl].x;
+          z.y += part[u][sl].y;
+          z.z += part[u][sl].z;
+          z.w += part[u][sl].w;
+        }
+        float *zr = &zred[0][tl][idx - tl * NP];
+        zr[0] = z.x;
+        zr[1] = z.y;
+        zr[2] = z.z;
+        zr[3] = z.w;
       }
     }
     __syncthreads();
