@@ -209,9 +209,9 @@ def main():
                "offsets": torch.empty((NN + 1,), dtype=torch.int32, device=dev),
                "perm": torch.empty((x.shape[0] * kk,), dtype=torch.int32, device=dev)}
 
-        def fn():
-            return ace.moe_forward(x, W, a_g, a_r, k=kk, tau=tau_, skip_disable=skip_disable, out=out, ws=ws,
-                                   want_plan=True)
+        # arguments checked and marshalled once; each call only enqueues the layer
+        fn = ace.prepare_forward(x, W, a_g, a_r, k=kk, tau=tau_, skip_disable=skip_disable, out=out, ws=ws,
+                                 want_plan=True)
         return fn, out
 
     def stack_leg():

@@ -6,6 +6,8 @@ the stream only; every step of the layer runs in the library's HIP kernels.
 """
 from __future__ import annotations
 
+import ctypes
+
 import torch
 
 from . import _lib
@@ -53,21 +55,10 @@ def workspace(desc: _lib.Desc, device) -> torch.Tensor:
     return buf
 
 
-def moe_forward(x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: int = 1,
-                eps: float = 1e-6, rms_eps: float = 1e-6, skip_disable: bool = False,
-                write_scores: bool = False, want_plan: bool = False, out: dict | None = None,
-                ws: torch.Tensor | None = None, fusion: str = "max") -> dict:
-    """One ACE MoE layer forward on the GPU.
-
-    x        [T, d] bf16 or fp32 device tensor (the layer input before RMSNorm)
-    weights  dict: gamma [d], w_router [N, d], b_router [N] fp32 or None,
-             w_gate / w_up [N, m, d], w_down [N, d, m], and optionally
-             ws_gate / ws_up [m_s, d], ws_down [d, m_s] (one shared expert)
-    a_gsp, a_rcr  [N] fp32 amplification tables
-    fusion   contribution rule: "max" (ACE) or an ablation variant
-             ("min", "mean", "gsp", "rcr", "score")
-    Returns dict(y, topk_idx, keep, gates[, scores][, counts, offsets, perm]).
-    """
+def _marshal(x, weights: dict, a_gsp, a_rcr, k, tau, m_min, eps, rms_eps, skip_disable, write_scores,
+             want_plan, out, ws, fusion):
+    """Check every tensor against the layer's shapes and build the C ABI structs.
+    Returns (desc, weights struct, outputs struct, output dict, workspace)."""
     dev = x.device
     T, d = x.shape
     dtype = x.dtype
@@ -116,11 +107,69 @@ def moe_forward(x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: in
                      _ptr(o.get("perm")))
     if ws is None:
         ws = workspace(desc, dev)
-    stream = torch.cuda.current_stream(dev).cuda_stream
+    return desc, W, O, o, ws
+
+
+def moe_forward(x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: int = 1,
+                eps: float = 1e-6, rms_eps: float = 1e-6, skip_disable: bool = False,
+                write_scores: bool = False, want_plan: bool = False, out: dict | None = None,
+                ws: torch.Tensor | None = None, fusion: str = "max") -> dict:
+    """One ACE MoE layer forward on the GPU.
+
+    x        [T, d] bf16 or fp32 device tensor (the layer input before RMSNorm)
+    weights  dict: gamma [d], w_router [N, d], b_router [N] fp32 or None,
+             w_gate / w_up [N, m, d], w_down [N, d, m], and optionally
+             ws_gate / ws_up [m_s, d], ws_down [d, m_s] (one shared expert)
+    a_gsp, a_rcr  [N] fp32 amplification tables
+    fusion   contribution rule: "max" (ACE) or an ablation variant
+             ("min", "mean", "gsp", "rcr", "score")
+    Returns dict(y, topk_idx, keep, gates[, scores][, counts, offsets, perm]).
+    """
+    desc, W, O, o, ws = _marshal(x, weights, a_gsp, a_rcr, k, tau, m_min, eps, rms_eps, skip_disable,
+                                 write_scores, want_plan, out, ws, fusion)
+    stream = torch.cuda.current_stream(x.device).cuda_stream
     st = _lib.forward_raw(desc, _ptr(x), W, O, _ptr(ws), ws.numel(), stream)
     if st != _lib.ACE_OK:
         raise _lib.AceError(st, _lib.status_string(st))
     return o
+
+
+class PreparedForward:
+    """A layer forward whose arguments are checked and marshalled once.
+
+    Calling it enqueues the layer on `stream` if one was given, else on the
+    current stream of the call, and returns the output dict; the tensors keep
+    their buffers, so a serving loop writes new tokens into `x` in place and
+    calls again.  Everything else is as in `moe_forward`."""
+
+    def __init__(self, x, weights: dict, a_gsp, a_rcr, *, k: int, tau: float, m_min: int = 1,
+                 eps: float = 1e-6, rms_eps: float = 1e-6, skip_disable: bool = False,
+                 write_scores: bool = False, want_plan: bool = False, out: dict | None = None,
+                 ws: torch.Tensor | None = None, fusion: str = "max", stream=None):
+        desc, W, O, o, ws = _marshal(x, weights, a_gsp, a_rcr, k, tau, m_min, eps, rms_eps, skip_disable,
+                                     write_scores, want_plan, out, ws, fusion)
+        # keep every tensor and struct alive for as long as this object
+        self._keep = (x, dict(weights), a_gsp, a_rcr, ws, desc, W, O, stream)
+        self.out = o
+        self._dev = x.device
+        self._fn = _lib.lib().ace_moe_forward
+        self._args = (ctypes.byref(desc), ctypes.c_void_p(_ptr(x)), ctypes.byref(W), ctypes.byref(O),
+                      ctypes.c_void_p(_ptr(ws)), ctypes.c_size_t(ws.numel()))
+        self._stream = None if stream is None else ctypes.c_void_p(stream.cuda_stream)
+
+    def __call__(self) -> dict:
+        s = self._stream
+        if s is None:
+            s = ctypes.c_void_p(torch.cuda.current_stream(self._dev).cuda_stream)
+        st = self._fn(*self._args, s)
+        if st != _lib.ACE_OK:
+            raise _lib.AceError(st, _lib.status_string(st))
+        return self.out
+
+
+def prepare_forward(x, weights: dict, a_gsp, a_rcr, **kw) -> PreparedForward:
+    """`PreparedForward` of these arguments (the keywords of `moe_forward`, plus `stream`)."""
+    return PreparedForward(x, weights, a_gsp, a_rcr, **kw)
 
 
 def tau_map(scores: torch.Tensor, qs, m_min: int = 1) -> dict:
