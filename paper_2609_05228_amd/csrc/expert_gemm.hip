@@ -164,8 +164,11 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   const int wr = wave >> 1, wc = wave & 1;
   const int K = GATEUP ? a.d : a.m;
   const bf16_t *act = static_cast<const bf16_t *>(a.act);
-  // A units this wave stages per stage (wave-uniform)
-  const int na = P::FA > wave ? (P::FA - wave + W - 1) / W : 0;
+  // A units this wave stages per stage (wave-uniform): only units holding a row of
+  // the tile (unit u covers rows 8u .. 8u+7); the MFMAs below skip row blocks past
+  // the tile too, and rows past the tile are never stored
+  const int fav = min(P::FA, (ti.rows + 7) >> 3);
+  const int na = fav > wave ? (fav - wave + W - 1) / W : 0;
   const int ur = lane >> 3;  // DMA lane -> row in its unit
 
   // A units this wave stages: u = wave + W j -> row block u / 2, row half u % 2 (= wave % 2)
@@ -254,6 +257,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
                                                     (h ? rd_off1 : rd_off0));
 #pragma unroll
       for (int i = 0; i < MW; ++i) {
+        if ((wr + RW * i) * 16 >= ti.rows) break;  // wave-uniform: row blocks past the tile
         const bf16x8_t av =
             *reinterpret_cast<const bf16x8_t *>(sa + (wr + RW * i) * 2 * kFragBytes + (h ? rd_off1 : rd_off0));
 #pragma unroll
