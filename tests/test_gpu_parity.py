@@ -287,3 +287,15 @@ def test_tau_extremes(tiny, tau):
         assert np.allclose(r["gpu"]["gates"], r["oracle"]["g"] / (1 + 1e-6), rtol=2e-6, atol=2e-7)
     else:
         assert keep[:, 0].all() and not keep[:, 1:].any()
+
+
+def test_large_batch():
+    """65536 tokens (4096 router chunks, hundreds of M tiles per GEMM launch):
+    every routing and skip decision and the whole plan against the oracle,
+    outputs on a token sample."""
+    L = synth.make_layer(synth.config("prefill_4096", T=65536, d=256, N=64, k=4, m=128, seed=41))
+    tb = oracle.tables.build_tables(L)
+    tau = _taus(L, tb["a_gsp"], tb["a_rcr"], [0.5])[0.5]
+    r = full_check(L, device_layer(L), tb["a_gsp"], tb["a_rcr"], tau, tokens=range(0, 65536, 997))
+    _report(f"large batch T=65536 tau={tau}", r)
+    assert abs((1 - r["gpu"]["keep"].mean()) - 0.5) < 1e-3
