@@ -119,6 +119,12 @@ struct GemmArgs {
   int dense_rows;         // > 0: dense single-group mode with this many rows
   int max_groups;         // upper bound of M tiles (grid sizing)
   int d, m;               // hidden and intermediate sizes of this GEMM's expert(s)
+  // A dense expert appended to the routed tiles (bf16 grouped GEMM): tiles
+  // n_tiles[0] .. n_tiles[0] + sh_tiles - 1 cover its rows (t - n_tiles[0]) * kTileM ..
+  // with the identity row map, its own operands and its own output.  0: none.
+  int sh_tiles, sh_rows;
+  const void *sh_act, *sh_w0, *sh_w1;
+  void *sh_out;
 };
 
 // Small-batch (decode) grouped GEMM: the same tiles, split over K into

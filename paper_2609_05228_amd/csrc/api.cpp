@@ -414,6 +414,24 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   gd.w0 = w->w_down;
   gd.w1 = nullptr;
   gd.out = at(L.Y);
+  // a shared expert with the routed experts' intermediate size runs as extra M tiles
+  // of the routed grouped GEMMs (one launch each instead of two half-filled ones)
+  const bool shared_in_routed = d.n_shared == 1 && bf16 && !L.skinny && d.m_shared == d.m;
+  if (shared_in_routed) {
+    const int st = L.dense_groups;
+    g.sh_tiles = gd.sh_tiles = st;
+    g.sh_rows = gd.sh_rows = d.T;
+    g.max_groups += st;
+    gd.max_groups += st;
+    g.sh_act = at(L.xn);
+    g.sh_w0 = w->ws_gate;
+    g.sh_w1 = w->ws_up;
+    g.sh_out = at(L.Hs);
+    gd.sh_act = at(L.Hs);
+    gd.sh_w0 = w->ws_down;
+    gd.sh_w1 = nullptr;
+    gd.sh_out = at(L.Ys);
+  }
   if (L.skinny) {
     const int slots = d.T * d.k;
     ace::SkinnyArgs su{g, L.splits_gu, slots, static_cast<float *>(at(L.part_g)), static_cast<float *>(at(L.part_u))};
@@ -428,8 +446,8 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   }
   mark(prof, 4, stream);
 
-  const void *Ys = nullptr;
-  if (d.n_shared == 1) {
+  const void *Ys = shared_in_routed ? at(L.Ys) : nullptr;
+  if (d.n_shared == 1 && !shared_in_routed) {
     ace::GemmArgs s{};
     s.act = at(L.xn);
     s.perm = nullptr;

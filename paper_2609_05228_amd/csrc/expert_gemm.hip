@@ -46,6 +46,7 @@ constexpr int kLdsBytes = 160 * 1024;
 struct TileInfo {
   int e, row0, rows;
   bool valid;
+  bool sh;  // a tile of the appended dense expert
 };
 
 __device__ __forceinline__ void map_block(int b, int nN, int *grp, int *nt) {
@@ -57,16 +58,25 @@ __device__ __forceinline__ void map_block(int b, int nN, int *grp, int *nt) {
 
 __device__ __forceinline__ TileInfo tile_info(const GemmArgs &a, int grp) {
   TileInfo ti;
+  ti.sh = false;
   if (a.dense_rows > 0) {
     ti.e = 0;
     ti.row0 = grp * kTileM;
     ti.rows = min(kTileM, a.dense_rows - ti.row0);
     ti.valid = ti.rows > 0;
   } else {
-    ti.valid = grp < a.n_tiles[0];
+    const int nr = a.n_tiles[0];
+    ti.valid = grp < nr;
     ti.e = ti.valid ? a.tile_expert[grp] : 0;
     ti.row0 = ti.valid ? a.tile_row0[grp] : 0;
     ti.rows = ti.valid ? a.tile_rows[grp] : 0;
+    if (!ti.valid && grp - nr < a.sh_tiles) {
+      ti.sh = true;
+      ti.e = 0;
+      ti.row0 = (grp - nr) * kTileM;
+      ti.rows = min(kTileM, a.sh_rows - ti.row0);
+      ti.valid = ti.rows > 0;
+    }
   }
   return ti;
 }
@@ -163,7 +173,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   const int r16 = lane & 15, g = lane >> 4;
   const int wr = wave >> 1, wc = wave & 1;
   const int K = GATEUP ? a.d : a.m;
-  const bf16_t *act = static_cast<const bf16_t *>(a.act);
+  // routed tile: the routed experts' operands; appended dense-expert tile: its own
+  const bf16_t *act = static_cast<const bf16_t *>(ti.sh ? a.sh_act : a.act);
+  const int32_t *perm = ti.sh ? nullptr : a.perm;
+  const void *w0 = ti.sh ? a.sh_w0 : a.w0;
+  const void *w1 = ti.sh ? a.sh_w1 : a.w1;
+  void *outp = ti.sh ? a.sh_out : a.out;
   // A units this wave stages per stage (wave-uniform): only units holding a row of
   // the tile (unit u covers rows 8u .. 8u+7); the MFMAs below skip row blocks past
   // the tile too, and rows past the tile are never stored
@@ -177,7 +192,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   for (int j = 0; j < NAM; ++j) {
     const int u = min(wave + W * j, P::FA - 1);
     const int row = min((u >> 1) * 16 + (u & 1) * 8 + ur, ti.rows - 1);  // rows past the tile repeat its last row
-    const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
+    const int src_row = perm ? perm[ti.row0 + row] : ti.row0 + row;
     asrc[j] = act + static_cast<size_t>(src_row) * K + 8 * unit_chunk(lane, u & 1);
   }
   // B units this wave stages: b = wave * NB + t -> block b / 2, row half t % 2
@@ -190,10 +205,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     const int c = 8 * unit_chunk(lane, j);
     if (GATEUP) {
       const size_t f = static_cast<size_t>(ti.e) * a.m + nt * BN + fg * 16 + 8 * j + ur;
-      bsrc[t] = static_cast<const bf16_t *>(cb ? a.w1 : a.w0) + f * a.d + c;
+      bsrc[t] = static_cast<const bf16_t *>(cb ? w1 : w0) + f * a.d + c;
     } else {
       const size_t n = static_cast<size_t>(ti.e) * a.d + nt * BN + fg * 32 + cb * 16 + 8 * j + ur;
-      bsrc[t] = static_cast<const bf16_t *>(a.w0) + n * a.m + c;
+      bsrc[t] = static_cast<const bf16_t *>(w0) + n * a.m + c;
     }
   }
   // fragment read offsets inside a 16-row block (two units) for k halves 0 and 1
@@ -272,7 +287,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   for (int fl = 0; fl < CW; ++fl) {
     const int grp = wc * CW + fl;
     if (GATEUP) {
-      bf16_t *H = static_cast<bf16_t *>(a.out);
+      bf16_t *H = static_cast<bf16_t *>(outp);
       const int f = nt * BN + grp * 16 + r16;
 #pragma unroll
       for (int i = 0; i < MW; ++i)
@@ -284,7 +299,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
                 f32_to_bf16(silu(acc[i][fl * 2][q]) * acc[i][fl * 2 + 1][q]);
         }
     } else {
-      bf16_t *Y = static_cast<bf16_t *>(a.out);
+      bf16_t *Y = static_cast<bf16_t *>(outp);
       const int n = nt * BN + grp * 32 + r16;
 #pragma unroll
       for (int i = 0; i < MW; ++i)
