@@ -12,8 +12,12 @@
 //     (each workgroup recomputes it; N <= 256), then every kept slot writes
 //     row = offsets[e] + chunk_base[e][g] + local_rank into perm and slot_row.
 //     Workgroup 0 also writes offsets and the M-tile list.
-// Integer work only, no atomics: the plan is bit-exact and independent of
-// scheduling.
+// When the [G, N] count matrix is at most 128 KB (and N a multiple of 4),
+// plan_kernel does both in one launch: each chunk workgroup reads the matrix and
+// derives the totals and its own chunk base itself.  Integer work only, no atomics: the plan is bit-exact
+// and independent of scheduling.
+#include <type_traits>
+
 #include "ace_internal.h"
 
 namespace ace {
@@ -130,11 +134,133 @@ __global__ __launch_bounds__(128) void scatter_kernel(PlanArgs a) {
   }
 }
 
+constexpr int kPlanMaxBytes = 128 * 1024;  // count matrix size up to which one kernel plans
+
+// One kernel for the whole plan when the [G, N] count matrix is small: every
+// chunk workgroup reads the whole matrix (L2-resident after the first reads) and
+// derives each expert's total and its own chunk base (the part of the column
+// before chunk g) itself, then scatters its kept slots.  Workgroup 0 also writes
+// counts, offsets and the M-tile list.  The same integers as expert_scan +
+// scatter, in one launch.
+//
+// Column sums: thread (r, w) reads V 32-bit words (4V experts) of chunk rows
+// r, r + R, ... and adds their bytes as packed 16-bit lanes (even bytes, odd
+// bytes); a chunk holds at most 16 tokens, so a lane stays below 16 * ceil(G / R)
+// (checked on the host).  The R row groups are then added per expert.
+template <int V>
+__global__ __launch_bounds__(256) void plan_kernel(PlanArgs a) {
+  __shared__ uint32_t red[4][256 * V];  // even/odd byte sums, then the same before chunk g
+  __shared__ int base[kMaxN];
+  __shared__ int cnt[kMaxN], off[kMaxN + 1], tcnt[kMaxN], toff[kMaxN + 1];
+  typedef typename std::conditional<V == 4, uint4, uint32_t>::type word_t;
+  const int tid = threadIdx.x;
+  const int N = a.N, G = a.G, g = blockIdx.x;
+  const int NW = N / 4;        // words per chunk row
+  const int W = NW / V;        // threads per chunk row
+  const int R = 256 / W;       // row groups
+  const int r = tid / W, w = tid - r * W;
+  if (r < R) {
+    uint32_t ev[V], od[V], pev[V], pod[V];
+#pragma unroll
+    for (int j = 0; j < V; ++j) ev[j] = od[j] = pev[j] = pod[j] = 0;
+    const word_t *src = reinterpret_cast<const word_t *>(a.chunk_count) + w;
+    for (int c0 = r; c0 < G; c0 += 8 * R) {
+      word_t q[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int c = c0 + u * R;
+        if (c < G) q[u] = src[static_cast<size_t>(c) * W];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int c = c0 + u * R;
+        if (c >= G) break;
+        const uint32_t before = c < g ? 0xffffffffu : 0u;
+        const uint32_t *qw = reinterpret_cast<const uint32_t *>(&q[u]);
+#pragma unroll
+        for (int j = 0; j < V; ++j) {
+          const uint32_t e0 = qw[j] & 0x00ff00ffu, o0 = (qw[j] >> 8) & 0x00ff00ffu;
+          ev[j] += e0;
+          od[j] += o0;
+          pev[j] += e0 & before;
+          pod[j] += o0 & before;
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < V; ++j) {
+      const int i = r * NW + w * V + j;
+      red[0][i] = ev[j];
+      red[1][i] = od[j];
+      red[2][i] = pev[j];
+      red[3][i] = pod[j];
+    }
+  }
+  __syncthreads();
+  if (tid < N) {
+    const int wi = tid >> 2, b = tid & 3;
+    const int q = b & 1, sh = 16 * (b >> 1);
+    int t = 0, p = 0;
+    for (int rr = 0; rr < R; ++rr) {
+      t += (red[q][rr * NW + wi] >> sh) & 0xffffu;
+      p += (red[q + 2][rr * NW + wi] >> sh) & 0xffffu;
+    }
+    cnt[tid] = t;
+    tcnt[tid] = (t + kTileM - 1) / kTileM;
+    base[tid] = p;
+  }
+  __syncthreads();
+  if (tid < 64) {
+    wave_scan_256(cnt, off, N, tid);
+    if (g == 0) wave_scan_256(tcnt, toff, N, tid);
+  }
+  __syncthreads();
+  if (g == 0) {
+    for (int e = tid; e < N; e += 256) {
+      a.counts[e] = cnt[e];
+      for (int j = 0; j < tcnt[e]; ++j) {
+        const int tg = toff[e] + j;
+        a.tile_expert[tg] = e;
+        a.tile_row0[tg] = off[e] + j * kTileM;
+        a.tile_rows[tg] = min(kTileM, cnt[e] - j * kTileM);
+      }
+    }
+    for (int e = tid; e <= N; e += 256) a.offsets[e] = off[e];
+    if (tid == 0) a.n_tiles[0] = toff[N];
+  }
+  // this chunk's kept slots: row = offsets[e] + chunk base of e + rank in the chunk
+  const int k = a.k;
+  if (tid < kRouteTokens * k) {
+    const int tl = tid / k;
+    const int t = g * kRouteTokens + tl;
+    if (t < a.T) {
+      const size_t o = static_cast<size_t>(t) * k + (tid - tl * k);
+      if (a.keep[o]) {
+        const int e = a.topk_idx[o];
+        const int row = off[e] + base[e] + a.local_rank[o];
+        a.perm[row] = t;
+        a.slot_row[o] = row;
+      }
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_plan(const PlanArgs &a, hipStream_t stream) {
-  expert_scan_kernel<<<dim3(a.N), 256, 0, stream>>>(a);
-  scatter_kernel<<<dim3(a.G), 128, 0, stream>>>(a);
+  // one-kernel plan: small matrix, rows of whole words, 16-bit lane sums that cannot overflow
+  const long long bytes = static_cast<long long>(a.G) * a.N;
+  const int V = a.N % 16 == 0 ? 4 : 1;
+  const int R = a.N % 4 == 0 ? 256 / (a.N / 4 / V) : 0;
+  if (bytes <= kPlanMaxBytes && R > 0 && 16LL * ((a.G + R - 1) / R) <= 0xffff) {
+    if (V == 4)
+      plan_kernel<4><<<dim3(a.G), 256, 0, stream>>>(a);
+    else
+      plan_kernel<1><<<dim3(a.G), 256, 0, stream>>>(a);
+  } else {
+    expert_scan_kernel<<<dim3(a.N), 256, 0, stream>>>(a);
+    scatter_kernel<<<dim3(a.G), 128, 0, stream>>>(a);
+  }
   return hipGetLastError();
 }
 
