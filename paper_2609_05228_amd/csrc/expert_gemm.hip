@@ -19,7 +19,8 @@
 //    and loads are issued only for the 16-row blocks a tile has;
 //  * operands move HBM/L2 -> LDS with global_load_lds_dwordx4 (no VGPR staging)
 //    through two LDS rings in 160 KB: activations (L2-resident) 2-4 K stages deep,
-//    expert weights (from HBM) 3-8 stages deep; each wave waits only for the
+//    expert weights (from HBM; with the non-temporal hint when no other M tile
+//    reads them) 3-8 stages deep; each wave waits only for the
 //    stage it computes next (vmcnt counted exactly from the issue schedule), then
 //    one barrier per K step;
 //  * one DMA instruction moves 8 rows x 128 bytes (whole cache lines) and lane i
@@ -46,7 +47,8 @@ constexpr int kLdsBytes = 160 * 1024;
 struct TileInfo {
   int e, row0, rows;
   bool valid;
-  bool sh;  // a tile of the appended dense expert
+  bool sh;    // a tile of the appended dense expert
+  bool once;  // no other M tile of this launch reads this tile's expert weights
 };
 
 __device__ __forceinline__ void map_block(int b, int nN, int *grp, int *nt) {
@@ -64,18 +66,23 @@ __device__ __forceinline__ TileInfo tile_info(const GemmArgs &a, int grp) {
     ti.row0 = grp * kTileM;
     ti.rows = min(kTileM, a.dense_rows - ti.row0);
     ti.valid = ti.rows > 0;
+    ti.once = a.dense_rows <= kTileM;
   } else {
     const int nr = a.n_tiles[0];
     ti.valid = grp < nr;
     ti.e = ti.valid ? a.tile_expert[grp] : 0;
     ti.row0 = ti.valid ? a.tile_row0[grp] : 0;
     ti.rows = ti.valid ? a.tile_rows[grp] : 0;
+    // an expert's tiles are consecutive in the list
+    ti.once = ti.valid && !(grp > 0 && a.tile_expert[grp - 1] == ti.e) &&
+              !(grp + 1 < nr && a.tile_expert[grp + 1] == ti.e);
     if (!ti.valid && grp - nr < a.sh_tiles) {
       ti.sh = true;
       ti.e = 0;
       ti.row0 = (grp - nr) * kTileM;
       ti.rows = min(kTileM, a.sh_rows - ti.row0);
       ti.valid = ti.rows > 0;
+      ti.once = a.sh_tiles == 1;
     }
   }
   return ti;
@@ -232,11 +239,22 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   // activation rows they all read are shared in their XCD's L2.
   const int k0 = mrot % nk;
   auto kofs = [&](int s) { return (s + k0 < nk ? s + k0 : s + k0 - nk) * BK; };
+  // weight units of stage s into LDS stage base st: weights that no other M tile
+  // reads stream with the non-temporal hint; weights shared by several M tiles
+  // (large experts, the dense expert's tiles) stay cacheable for the other tiles
+  auto issue_b = [&](uint32_t st, int s) {
+    if (ti.once) {
+#pragma unroll
+      for (int t = 0; t < NB; ++t) dma16_stream(bsrc[t] + kofs(s), st + (wave * NB + t) * kFragBytes);
+    } else {
+#pragma unroll
+      for (int t = 0; t < NB; ++t) dma16(bsrc[t] + kofs(s), st + (wave * NB + t) * kFragBytes);
+    }
+  };
   // prologue: B stages 0..SB-2, then A stages 0..SA-2
   for (int s = 0; s < SB - 1 && s < nk; ++s) {
     const uint32_t st = ldsB + s * P::BSZ;
-#pragma unroll
-    for (int t = 0; t < NB; ++t) dma16(bsrc[t] + kofs(s), st + (wave * NB + t) * kFragBytes);
+    issue_b(st, s);
   }
   for (int s = 0; s < SA - 1 && s < nk; ++s) {
     const uint32_t st = ldsA + s * P::ASZ;
@@ -258,8 +276,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     if (kt + SB - 1 < nk) {
       const int s = kt + SB - 1;
       const uint32_t st = ldsB + (s % SB) * P::BSZ;
-#pragma unroll
-      for (int t = 0; t < NB; ++t) dma16(bsrc[t] + kofs(s), st + (wave * NB + t) * kFragBytes);
+      issue_b(st, s);
     }
     const uint8_t *sa = smemA + (kt % SA) * P::ASZ;
     const uint8_t *sb = smemB + (kt % SB) * P::BSZ;

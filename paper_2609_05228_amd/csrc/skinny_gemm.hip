@@ -5,7 +5,9 @@
 //    block and an up block) or 32 output columns (down) x one K split;
 //  * the wave streams its weight rows and its activation rows into a private
 //    LDS ring with global_load_lds_dwordx4, one 8-row x 128-byte unit per
-//    instruction (whole cache lines; see lds_dma.h), P stages of 64 k deep, and
+//    instruction (whole cache lines; see lds_dma.h; weights carry the
+//    non-temporal hint when the wave makes one pass over them), P stages of 64 k
+//    deep, and
 //    waits only on its own vmcnt: no barriers, waves run independently;
 //  * it reads MFMA fragments back from the ring and multiplies them with
 //    v_mfma_f32_16x16x32_bf16;
@@ -61,7 +63,7 @@ constexpr bool kSkinnyTwoBlocks = kSkinnyRingBytes / ((4 + 4) * kUnitBytes) >= 2
 
 template <bool GATEUP, int MB, int AU>
 __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo &ti, int nb, int s, int rot,
-                                            uint8_t *ring) {
+                                            bool once, uint8_t *ring) {
   static_assert(AU == 2 * MB || (MB == 1 && AU == 1), "activation units cover the row blocks");
   using R = SkinnyRing<AU>;
   constexpr int P = R::P, NU = R::NU;
@@ -106,8 +108,16 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
   auto issue = [&](int st) {
     const uint32_t base = ring_lds + (st % P) * R::STAGE;
     const int kb = st + k0 < nk ? st + k0 : st + k0 - nk;
+    // weights: non-temporal when this is the item's only pass over them
+    if (once) {
 #pragma unroll
-    for (int t = 0; t < NU; ++t) dma16(src[t] + kb * 64, base + t * kUnitBytes);
+      for (int t = 0; t < 4; ++t) dma16_stream(src[t] + kb * 64, base + t * kUnitBytes);
+    } else {
+#pragma unroll
+      for (int t = 0; t < 4; ++t) dma16(src[t] + kb * 64, base + t * kUnitBytes);
+    }
+#pragma unroll
+    for (int t = 4; t < NU; ++t) dma16(src[t] + kb * 64, base + t * kUnitBytes);  // activation rows
   };
 
   f32x4_t acc[MB][2];
@@ -197,14 +207,14 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
   const int blocks = (ti.rows + 15) >> 4;
   const int rot = static_cast<int>(item & 0x7fffffff);
   if (ti.rows <= 8) {
-    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, rot, ring);
+    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, rot, true, ring);
   } else if (blocks <= 1 || !kSkinnyTwoBlocks) {
     // 16 rows per pass (more than 16 rows re-read the weights, mostly from L2)
     for (int r = 0; r < ti.rows; r += 16) {
       TileInfo part = ti;
       part.row0 = ti.row0 + r;
       part.rows = min(16, ti.rows - r);
-      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, rot, ring);
+      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, rot, ti.rows <= 16, ring);
     }
   } else if constexpr (kSkinnyTwoBlocks) {
     // 32 rows per pass
@@ -212,7 +222,7 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
       TileInfo part = ti;
       part.row0 = ti.row0 + r;
       part.rows = min(32, ti.rows - r);
-      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, rot, ring);
+      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, rot, ti.rows <= 32, ring);
     }
   }
 }
