@@ -43,6 +43,15 @@ template <> struct Elem<bf16_t> {
   static __device__ __forceinline__ bf16_t from_f32(float v) { return f32_to_bf16(v); }
 };
 
+// SiLU of a value whose product with the up projection is rounded to bf16 right
+// after: the hardware base-2 exponential and reciprocal (each about 1 ulp of
+// fp32, far below bf16's 8-bit significand) instead of an exact division.
+// v -> -inf gives -0, v -> +inf gives v.  fp32 layers keep the exact form.
+__device__ __forceinline__ float silu_for_bf16(float v) {
+  const float e = __builtin_amdgcn_exp2f(v * -1.4426950408889634f);  // exp(-v)
+  return v * __builtin_amdgcn_rcpf(1.0f + e);
+}
+
 constexpr int kMaxN = 256;   // routed experts supported by the router kernel
 constexpr int kMaxK = 8;     // top-k supported by the router kernel
 constexpr int kTileM = 256;  // rows of one grouped-GEMM M tile (the dispatch plan's tile size)

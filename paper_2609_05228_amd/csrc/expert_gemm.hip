@@ -88,7 +88,7 @@ __device__ __forceinline__ TileInfo tile_info(const GemmArgs &a, int grp) {
   return ti;
 }
 
-__device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }
+__device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }  // fp32 layers
 
 
 constexpr int kGemmWaves = 8;  // waves per workgroup (two per SIMD)
@@ -313,7 +313,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
           const int row = (wr + RW * i) * 16 + 4 * g + q;
           if (row < ti.rows)
             H[static_cast<size_t>(ti.row0 + row) * a.m + f] =
-                f32_to_bf16(silu(acc[i][fl * 2][q]) * acc[i][fl * 2 + 1][q]);
+                f32_to_bf16(silu_for_bf16(acc[i][fl * 2][q]) * acc[i][fl * 2 + 1][q]);
         }
     } else {
       bf16_t *Y = static_cast<bf16_t *>(outp);

@@ -42,8 +42,6 @@ __device__ __forceinline__ TileInfo skinny_tile(const GemmArgs &a, int grp) {
   return ti;
 }
 
-__device__ __forceinline__ float silu(float v) { return v / (1.0f + expf(-v)); }
-
 constexpr int kSkinnyWavesPerGroup = 4;
 constexpr int kSkinnyRingBytes = 20 * 1024;  // LDS ring of one wave (4 waves: 80 KB, two workgroups per CU)
 
@@ -167,7 +165,7 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
       if (GATEUP) {
         const int f = nb * 16 + r16;
         if (sa.splits == 1) {
-          static_cast<bf16_t *>(a.out)[r * a.m + f] = f32_to_bf16(silu(acc[mi][0][q]) * acc[mi][1][q]);
+          static_cast<bf16_t *>(a.out)[r * a.m + f] = f32_to_bf16(silu_for_bf16(acc[mi][0][q]) * acc[mi][1][q]);
         } else {
           const size_t o = (static_cast<size_t>(s) * sa.rows_cap + r) * a.m + f;
           sa.part0[o] = acc[mi][0][q];
@@ -241,7 +239,7 @@ __global__ __launch_bounds__(256) void swiglu_reduce_kernel(SkinnyArgs sa, const
       gs += sa.part0[s * plane + i];
       us += sa.part1[s * plane + i];
     }
-    H[i] = f32_to_bf16(silu(gs) * us);
+    H[i] = f32_to_bf16(silu_for_bf16(gs) * us);
   }
 }
 
