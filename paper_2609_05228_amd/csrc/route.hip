@@ -276,7 +276,7 @@ __device__ __forceinline__ void accumulate_logits(const T *xrow, const T *gl, co
 
 // One wave's partial logits of blocks jfirst, jfirst + step, ... < jend for
 // the 16 tokens from t0, into zred[token][expert] and ssred[token] (LDS).
-template <typename T, int NT, int ZS>
+template <typename T, int NT, int ZS, bool ONE_BLOCK_PATH>
 __device__ __forceinline__ void wave_logits(const RouteArgs &a, int t0, int jfirst, int jend, int step, int rot,
                                             float (*zred)[ZS], float *ssred) {
   const T *x = static_cast<const T *>(a.x);
@@ -299,7 +299,14 @@ __device__ __forceinline__ void wave_logits(const RouteArgs &a, int t0, int jfir
 #pragma unroll
   for (int f = 0; f < NT; ++f) acc[f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float ss = 0.f;
-  accumulate_logits<T, NT>(xrow, gl, wl, woff, jfirst, jend, step, rot, acc, ss);
+  if (ONE_BLOCK_PATH && jfirst < jend && jfirst + step >= jend) {
+    // exactly one block (decode-sized K slices): one load round, no repeats
+    Stage<T, NT> st;
+    load_stage<T, NT>(st, xrow, gl, wl, woff, 32 * jfirst);
+    mma_stage<NT>(st, acc, ss, true);
+  } else {
+    accumulate_logits<T, NT>(xrow, gl, wl, woff, jfirst, jend, step, rot, acc, ss);
+  }
   // D[row = token 4 grp + i][col = expert 16 f + r16]
 #pragma unroll
   for (int f = 0; f < NT; ++f)
@@ -327,7 +334,8 @@ __global__ __launch_bounds__(256) void route_partial_kernel(RouteArgs a) {
   const int s = blockIdx.y;
   const int nbs = (a.d >> 5) / a.ksplit;  // blocks per slice
   if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) a.ticket[0] = 0u;  // for the select kernel's plan
-  wave_logits<T, NT, NP + 1>(a, t0, s * nbs + wave, (s + 1) * nbs, kPartWaves, blockIdx.x, zred[wave], ssred[wave]);
+  wave_logits<T, NT, NP + 1, true>(a, t0, s * nbs + wave, (s + 1) * nbs, kPartWaves, blockIdx.x, zred[wave],
+                                   ssred[wave]);
   __syncthreads();
   const size_t plane = static_cast<size_t>(s) * a.T;
   for (int idx = tid; idx < kTok * NP; idx += 256) {
@@ -586,7 +594,7 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   } else {
     // ---- 1. logits over all K: wave w takes blocks w, w + 8, ...
     // workgroups are dealt to the 8 XCDs round-robin: rotate by the index on the XCD
-    wave_logits<T, NT, NP + 1>(a, t0, wave, d >> 5, kWaves, blockIdx.x >> 3, zred[wave], ssred[wave]);
+    wave_logits<T, NT, NP + 1, false>(a, t0, wave, d >> 5, kWaves, blockIdx.x >> 3, zred[wave], ssred[wave]);
     __syncthreads();
     if (tid < kTok) {
       float ssum = 0.f;
