@@ -57,7 +57,7 @@ constexpr int kMaxK = 8;     // top-k supported by the router kernel
 constexpr int kTileM = 256;  // rows of one grouped-GEMM M tile (the dispatch plan's tile size)
 constexpr int kRouteTokens = 16;  // tokens per router workgroup (one dispatch-plan chunk)
 constexpr int kRouteMaxSlices = 16;  // K slices of the small-batch router
-constexpr int kRouteMaxSplitChunks = 16;  // chunks of the small-batch (split) router path
+constexpr int kRouteMaxSplitChunks = 16;  // most chunks that take the small-batch (K-slice) router path
 
 // 16-expert tiles the router kernels are compiled for: 1, 2, 4, 8 or 16 (>= N / 16)
 inline int route_expert_tiles(int N) {
@@ -84,8 +84,7 @@ struct RouteArgs {
   float *zpart;           // [ksplit, T, zstride]: partial logits of the K slices (ksplit > 0)
   float *sspart;          // [ksplit, T]: partial sums of squares of x
   int ksplit;             // 0: one fused kernel; else K slices (<= 16, dividing d / 32)
-  // small batches (ksplit > 0): the last select workgroup also writes the dispatch plan
-  uint32_t *ticket;       // completed-workgroup counter, zeroed by route_partial_kernel
+  // one chunk (T <= 16): the select workgroup also writes the dispatch plan
   int32_t *counts;        // [N]
   int32_t *offsets;       // [N+1]
   int32_t *perm;          // [T*k]

@@ -35,7 +35,7 @@ int pick_splits(long items, int K) {
 }
 
 struct Layout {
-  size_t xn, zpart, sspart, ticket, local_rank, chunk_count, chunk_base, slot_row, gates, counts, offsets, perm;
+  size_t xn, zpart, sspart, local_rank, chunk_count, chunk_base, slot_row, gates, counts, offsets, perm;
   size_t tile_e, tile_r0, tile_rows, n_tiles, H, Y, Hs, Ys, part_g, part_u, part_y, total;
   int G, max_groups, dense_groups;
   bool skinny;          // small-batch path (bf16, T <= kSkinnyMaxT)
@@ -52,7 +52,7 @@ Layout layout_for(const ace_moe_desc &d) {
   L.G = static_cast<int>((T + ace::kRouteTokens - 1) / ace::kRouteTokens);
   // router: small batches spread W_r over (chunk, K slice) workgroups
   L.ksplit = 0;
-  if (L.G <= 16) {
+  if (L.G <= ace::kRouteMaxSplitChunks) {
     const int nb = d.d / 32;
     L.ksplit = 1;
     while (L.ksplit < ace::kRouteMaxSlices && nb % (2 * L.ksplit) == 0 && L.G * L.ksplit < 128) L.ksplit *= 2;
@@ -76,7 +76,6 @@ Layout layout_for(const ace_moe_desc &d) {
   L.xn = take(T * dd * esz);
   L.zpart = take(static_cast<size_t>(L.ksplit) * T * L.zstride * 4);
   L.sspart = take(static_cast<size_t>(L.ksplit) * T * 4);
-  L.ticket = take(4);
   L.local_rank = take(slots);
   L.chunk_count = take(static_cast<size_t>(L.G) * N);
   L.chunk_base = take(static_cast<size_t>(L.G) * N * 4);
@@ -350,7 +349,6 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   ra.zpart = static_cast<float *>(at(L.zpart));
   ra.sspart = static_cast<float *>(at(L.sspart));
   ra.ksplit = L.ksplit;
-  ra.ticket = static_cast<uint32_t *>(at(L.ticket));
   ra.counts = counts;
   ra.offsets = offsets;
   ra.perm = perm;
@@ -390,8 +388,9 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   pa.k = d.k;
   pa.N = d.N;
   pa.G = L.G;
-  // small batches: the router's last select workgroup already wrote the plan
-  if (L.ksplit == 0 && ace::launch_plan(pa, stream) != hipSuccess) return ACE_ERR_HIP;
+  // one chunk: the router's select workgroup already wrote the plan
+  const bool planned = L.ksplit > 0 && L.G == 1;
+  if (!planned && ace::launch_plan(pa, stream) != hipSuccess) return ACE_ERR_HIP;
   mark(prof, 2, stream);
 
   ace::GemmArgs g{};

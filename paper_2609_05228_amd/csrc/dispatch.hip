@@ -159,6 +159,16 @@ __global__ __launch_bounds__(256) void plan_kernel(PlanArgs a) {
   const int W = NW / V;        // threads per chunk row
   const int R = 256 / W;       // row groups
   const int r = tid / W, w = tid - r * W;
+  // this thread's slot of the chunk (thread tid < 16 k): its routing, loaded
+  // now so the loads overlap the column sums below
+  const int k = a.k;
+  const int tl = tid / k;
+  const int t = g * kRouteTokens + tl;
+  const bool has_slot = tid < kRouteTokens * k && t < a.T;
+  const size_t o = static_cast<size_t>(t) * k + (tid - tl * k);
+  const bool kept = has_slot && a.keep[o];
+  const int e_slot = has_slot ? a.topk_idx[o] : 0;
+  const int rank = has_slot ? a.local_rank[o] : 0;
   if (r < R) {
     uint32_t ev[V], od[V], pev[V], pod[V];
 #pragma unroll
@@ -229,19 +239,10 @@ __global__ __launch_bounds__(256) void plan_kernel(PlanArgs a) {
     if (tid == 0) a.n_tiles[0] = toff[N];
   }
   // this chunk's kept slots: row = offsets[e] + chunk base of e + rank in the chunk
-  const int k = a.k;
-  if (tid < kRouteTokens * k) {
-    const int tl = tid / k;
-    const int t = g * kRouteTokens + tl;
-    if (t < a.T) {
-      const size_t o = static_cast<size_t>(t) * k + (tid - tl * k);
-      if (a.keep[o]) {
-        const int e = a.topk_idx[o];
-        const int row = off[e] + base[e] + a.local_rank[o];
-        a.perm[row] = t;
-        a.slot_row[o] = row;
-      }
-    }
+  if (kept) {
+    const int row = off[e_slot] + base[e_slot] + rank;
+    a.perm[row] = t;
+    a.slot_row[o] = row;
   }
 }
 

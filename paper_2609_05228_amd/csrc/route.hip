@@ -333,7 +333,6 @@ __global__ __launch_bounds__(256) void route_partial_kernel(RouteArgs a) {
   const int t0 = blockIdx.x * kTok;
   const int s = blockIdx.y;
   const int nbs = (a.d >> 5) / a.ksplit;  // blocks per slice
-  if (blockIdx.x == 0 && blockIdx.y == 0 && tid == 0) a.ticket[0] = 0u;  // for the select kernel's plan
   wave_logits<T, NT, NP + 1, true>(a, t0, s * nbs + wave, (s + 1) * nbs, kPartWaves, blockIdx.x, zred[wave],
                                    ssred[wave]);
   __syncthreads();
@@ -355,105 +354,11 @@ __global__ __launch_bounds__(256) void route_partial_kernel(RouteArgs a) {
   }
 }
 
-// Small batches (at most 16 chunks): the select workgroup that finishes last
-// writes the whole dispatch plan, so no plan kernels follow.  Each workgroup
-// publishes its chunk (counts, ranks, routing) with a device-scope fence before
-// taking a ticket; the last one fences again (its L1 then holds no stale lines)
-// and computes, from integers only: counts, their exclusive scan (offsets), the
-// M-tile list, and row = offsets[e] + (kept slots of e in earlier chunks) +
-// rank for every kept slot.  The result does not depend on which workgroup is
-// last.
-__device__ __forceinline__ void plan_if_last(const RouteArgs &a) {
-  __shared__ int last;
-  __shared__ int cnt[kMaxN], off[kMaxN + 1], tcnt[kMaxN], toff[kMaxN + 1];
-  __shared__ int base[kRouteMaxSplitChunks][kMaxN];  // kept slots of e in chunks before g
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int N = a.N, G = gridDim.x;
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) last = atomicAdd(a.ticket, 1u) == static_cast<uint32_t>(G - 1);
-  __syncthreads();
-  if (!last) return;
-  __threadfence();
-  for (int e = tid; e < N; e += 512) {
-    int c[kRouteMaxSplitChunks];
-#pragma unroll
-    for (int g = 0; g < kRouteMaxSplitChunks; ++g) c[g] = g < G ? a.chunk_count[static_cast<size_t>(g) * N + e] : 0;
-    int run = 0;
-#pragma unroll
-    for (int g = 0; g < kRouteMaxSplitChunks; ++g) {
-      if (g < G) base[g][e] = run;
-      run += c[g];
-    }
-    cnt[e] = run;
-    tcnt[e] = (run + kTileM - 1) / kTileM;
-  }
-  __syncthreads();
-  if (tid < 64) {
-    // exclusive scans of the counts and tile counts (N <= 256: four per lane)
-    int s = 0, st = 0, loc[4], loct[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = lane * 4 + j;
-      loc[j] = s;
-      loct[j] = st;
-      s += e < N ? cnt[e] : 0;
-      st += e < N ? tcnt[e] : 0;
-    }
-    int inc = s, inct = st;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-      const int v = __shfl_up(inc, o), vt = __shfl_up(inct, o);
-      if (lane >= o) {
-        inc += v;
-        inct += vt;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int e = lane * 4 + j;
-      if (e < N) {
-        off[e] = inc - s + loc[j];
-        toff[e] = inct - st + loct[j];
-      }
-    }
-    if (lane == 63) {
-      off[N] = inc;
-      toff[N] = inct;
-    }
-  }
-  __syncthreads();
-  for (int e = tid; e < N; e += 512) {
-    a.counts[e] = cnt[e];
-    a.offsets[e] = off[e];
-    for (int j = 0; j < tcnt[e]; ++j) {
-      const int tg = toff[e] + j;
-      a.tile_expert[tg] = e;
-      a.tile_row0[tg] = off[e] + j * kTileM;
-      a.tile_rows[tg] = min(kTileM, cnt[e] - j * kTileM);
-    }
-  }
-  if (tid == 0) {
-    a.offsets[N] = off[N];
-    a.n_tiles[0] = toff[N];
-  }
-  const int slots = a.T * a.k;
-  for (int o = tid; o < slots; o += 512) {
-    const bool kept = a.keep[o] != 0;
-    const int e = a.topk_idx[o];
-    const int rank = a.local_rank[o];
-    if (!kept) continue;
-    const int t = o / a.k;
-    const int row = off[e] + base[t / kTok][e] + rank;
-    a.perm[row] = t;
-    a.slot_row[o] = row;
-  }
-}
-
 // One chunk (at most 16 tokens): its only select workgroup writes the plan
 // straight from the per-expert token masks in LDS and each kept slot's rank
-// (held by the slot's own lane), with no fence, ticket or global re-read.  Same
-// rows as plan_if_last: row = offsets[e] + rank.
+// (held by the slot's own lane), with no global re-read: row = offsets[e] +
+// rank, the rows the plan kernels give.  Several chunks: the plan kernels of
+// dispatch.hip follow.
 __device__ __forceinline__ void plan_one_chunk(const RouteArgs &a, const uint32_t *emask, bool kept, int e_mine,
                                                int t, int sub, int rank) {
   __shared__ int off1[kMaxN + 1];
@@ -735,7 +640,6 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   if (my_kept) a.local_rank[static_cast<size_t>(t) * a.k + sub] = static_cast<uint8_t>(my_rank);
   for (int e = tid; e < N; e += 512)
     a.chunk_count[static_cast<size_t>(blockIdx.x) * N + e] = static_cast<uint8_t>(__popc(emask[e]));
-  if constexpr (SPLIT) plan_if_last(a);
 }
 
 template <typename T, int NT>
