@@ -143,6 +143,19 @@ struct SkinnyArgs {
   int rows_cap;    // row capacity of a partial-sum plane (T * k)
   float *part0;    // gate/up: gate partials [splits, rows_cap, m]; down: Y partials [splits, rows_cap, d]
   float *part1;    // gate/up: up partials [splits, rows_cap, m]
+  // self_plan (routed gate/up, 2-4 router chunks): each wave derives its tile (the
+  // grp-th expert with kept slots) and the tokens of its rows from the router's
+  // per-chunk counts and the routing, instead of reading a plan; one item per
+  // tile writes its slots' rows (slot_row, perm), item 0 writes counts, offsets
+  // and the tile list (into the buffers g's tile pointers name) that the down
+  // kernel reads
+  bool self_plan;
+  const int32_t *topk_idx;     // [T, k]
+  const uint8_t *keep;         // [T, k]
+  const uint8_t *chunk_count;  // [G, N]
+  int32_t *counts, *offsets, *perm, *slot_row;
+  int32_t *tile_expert, *tile_row0, *tile_rows, *n_tiles;
+  int T, k, N, G;
 };
 
 struct CombineArgs {

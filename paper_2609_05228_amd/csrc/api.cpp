@@ -388,8 +388,10 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   pa.k = d.k;
   pa.N = d.N;
   pa.G = L.G;
-  // one chunk: the router's select workgroup already wrote the plan
-  const bool planned = L.ksplit > 0 && L.G == 1;
+  // one chunk: the router's select workgroup already wrote the plan; several chunks of a
+  // small bf16 batch: the skinny gate/up kernel derives it (SkinnyArgs::self_plan)
+  const bool self_plan = L.skinny && L.G > 1;
+  const bool planned = (L.ksplit > 0 && L.G == 1) || self_plan;
   if (!planned && ace::launch_plan(pa, stream) != hipSuccess) return ACE_ERR_HIP;
   mark(prof, 2, stream);
 
@@ -434,6 +436,24 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   if (L.skinny) {
     const int slots = d.T * d.k;
     ace::SkinnyArgs su{g, L.splits_gu, slots, static_cast<float *>(at(L.part_g)), static_cast<float *>(at(L.part_u))};
+    if (self_plan) {
+      su.self_plan = true;
+      su.topk_idx = out->topk_idx;
+      su.keep = out->keep;
+      su.chunk_count = chunk_count;
+      su.counts = counts;
+      su.offsets = offsets;
+      su.perm = perm;
+      su.slot_row = slot_row;
+      su.tile_expert = tile_e;
+      su.tile_row0 = tile_r0;
+      su.tile_rows = tile_rows;
+      su.n_tiles = n_tiles;
+      su.T = d.T;
+      su.k = d.k;
+      su.N = d.N;
+      su.G = L.G;
+    }
     if (ace::launch_skinny(su, true, offsets + d.N, stream) != hipSuccess) return ACE_ERR_HIP;
     mark(prof, 3, stream);
     ace::SkinnyArgs sd{gd, L.splits_dn, slots, static_cast<float *>(at(L.part_y)), nullptr};

@@ -26,6 +26,125 @@ struct TileInfo {
   bool valid;
 };
 
+// Tile grp of the dispatch plan derived by this wave (SkinnyArgs::self_plan).
+// Lane l holds experts 4l .. 4l+3: their kept-slot counts (summed over the G
+// chunks) give, by wave scans, the experts with kept slots in id order (tile
+// grp is the grp-th of them) and their row offsets.  Lane t (t < T <= 64) finds
+// the slot of token t routed to the tile's expert, if kept; ranks in token
+// order give the rows, and lane r receives the token of row r (*tok).  The same
+// integers as the plan kernels: rows in (expert, token) order.
+__device__ TileInfo self_tile(const SkinnyArgs &sa, int grp, bool write_slots, bool write_plan, int *tok) {
+  const int lane = threadIdx.x & 63;
+  const int N = sa.N;
+  // routing of token `lane` (issued first: independent of the counts)
+  int te[kMaxK];
+  uint8_t tk[kMaxK];
+#pragma unroll
+  for (int i = 0; i < kMaxK; ++i) {
+    const bool in = lane < sa.T && i < sa.k;
+    const size_t o = static_cast<size_t>(lane) * sa.k + i;
+    te[i] = in ? sa.topk_idx[o] : -1;
+    tk[i] = in ? sa.keep[o] : 0;
+  }
+  int c[4] = {0, 0, 0, 0};
+  if ((N & 3) == 0) {
+    // four experts per 32-bit word (rows of N bytes stay 4-byte aligned)
+    for (int g = 0; g < sa.G; ++g) {
+      const uint32_t w = 4 * lane < N ? reinterpret_cast<const uint32_t *>(sa.chunk_count + static_cast<size_t>(g) * N)[lane] : 0u;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) c[j] += (w >> (8 * j)) & 0xFFu;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = 4 * lane + j;
+      for (int g = 0; g < sa.G; ++g) c[j] += e < N ? sa.chunk_count[static_cast<size_t>(g) * N + e] : 0;
+    }
+  }
+  const int na = (c[0] > 0) + (c[1] > 0) + (c[2] > 0) + (c[3] > 0);
+  const int ns = c[0] + c[1] + c[2] + c[3];
+  int na_inc = na, ns_inc = ns;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int va = __shfl_up(na_inc, o), vs = __shfl_up(ns_inc, o);
+    if (lane >= o) {
+      na_inc += va;
+      ns_inc += vs;
+    }
+  }
+  const int na_ex = na_inc - na, ns_ex = ns_inc - ns;
+  const int n_active = __shfl(na_inc, 63);
+  if (write_plan) {
+    int off = ns_ex, a_idx = na_ex;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int e = 4 * lane + j;
+      if (e < N) {
+        sa.counts[e] = c[j];
+        sa.offsets[e] = off;
+        if (c[j] > 0) {
+          sa.tile_expert[a_idx] = e;
+          sa.tile_row0[a_idx] = off;
+          sa.tile_rows[a_idx] = c[j];
+          ++a_idx;
+        }
+      }
+      off += c[j];
+    }
+    if (lane == 63) {
+      sa.offsets[N] = ns_inc;
+      sa.n_tiles[0] = n_active;
+    }
+  }
+  TileInfo ti;
+  ti.valid = grp < n_active;
+  if (!ti.valid) {
+    ti.e = ti.row0 = ti.rows = 0;
+    *tok = 0;
+    return ti;
+  }
+  // the lane holding tile grp's expert, then the expert among its four
+  const unsigned long long owner = __ballot(na_ex <= grp && grp < na_inc);
+  const int L = __ffsll(static_cast<long long>(owner)) - 1;
+  int e_l = 0, r0_l = ns_ex, rows_l = 0, q = grp - na_ex, found = 0;
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (!found && c[j] > 0) {
+      if (q == 0) {
+        e_l = 4 * lane + j;
+        rows_l = c[j];
+        found = 1;
+      } else {
+        --q;
+        r0_l += c[j];
+      }
+    } else if (!found) {
+      r0_l += c[j];
+    }
+  }
+  ti.e = __shfl(e_l, L);
+  ti.row0 = __shfl(r0_l, L);
+  ti.rows = __shfl(rows_l, L);
+  // tokens of the tile's rows
+  int slot = -1;
+#pragma unroll
+  for (int i = 0; i < kMaxK; ++i)
+    if (te[i] == ti.e && tk[i]) slot = i;
+  const bool hit = slot >= 0;
+  const unsigned long long hits = __ballot(hit);
+  const int rank = __popcll(hits & ((1ull << lane) - 1ull));
+  // a permutation of the 64 lanes (hits to 0 .. n-1 in token order, the others
+  // after them), so every lane receives exactly one value: lane r <- token of row r
+  const int dst = hit ? rank : __popcll(hits) + (lane - rank);
+  *tok = __builtin_amdgcn_ds_permute(dst << 2, lane);
+  if (write_slots && hit) {
+    const int row = ti.row0 + rank;
+    sa.slot_row[static_cast<size_t>(lane) * sa.k + slot] = row;
+    sa.perm[row] = lane;
+  }
+  return ti;
+}
+
 __device__ __forceinline__ TileInfo skinny_tile(const GemmArgs &a, int grp) {
   TileInfo ti;
   if (a.dense_rows > 0) {
@@ -61,7 +180,7 @@ constexpr bool kSkinnyTwoBlocks = kSkinnyRingBytes / ((4 + 4) * kUnitBytes) >= 2
 
 template <bool GATEUP, int MB, int AU>
 __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo &ti, int nb, int s, int rot,
-                                            bool once, uint8_t *ring) {
+                                            bool once, int tok, int rbase, uint8_t *ring) {
   static_assert(AU == 2 * MB || (MB == 1 && AU == 1), "activation units cover the row blocks");
   using R = SkinnyRing<AU>;
   constexpr int P = R::P, NU = R::NU;
@@ -94,7 +213,9 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
   for (int t = 4; t < NU; ++t) {
     const int mi = (t - 4) >> 1, j = t & 1;
     const int row = min(mi * 16 + 8 * j + ur, ti.rows - 1);  // rows past the tile repeat its last row
-    const int src_row = a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
+    // self_plan: the token of tile row r sits in lane r of tok (tile rows <= 64;
+    // this item covers tile rows rbase ..)
+    const int src_row = sa.self_plan ? __shfl(tok, rbase + row) : a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
     src[t] = act + static_cast<size_t>(src_row) * K + kbase + 8 * unit_chunk(lane, j);
   }
   const uint32_t ring_lds = lds_addr(ring);
@@ -200,19 +321,21 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
   const int s = static_cast<int>(rest % sa.splits);
   const int grp = static_cast<int>(rest / sa.splits);
   if (grp >= a.max_groups) return;
-  const TileInfo ti = skinny_tile(a, grp);
+  int tok = 0;
+  const TileInfo ti = (GATEUP && sa.self_plan) ? self_tile(sa, grp, nb == 0 && s == 0, item == 0, &tok)
+                                              : skinny_tile(a, grp);
   if (!ti.valid) return;
   const int blocks = (ti.rows + 15) >> 4;
   const int rot = static_cast<int>(item & 0x7fffffff);
   if (ti.rows <= 8) {
-    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, rot, true, ring);
+    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, rot, true, tok, 0, ring);
   } else if (blocks <= 1 || !kSkinnyTwoBlocks) {
     // 16 rows per pass (more than 16 rows re-read the weights, mostly from L2)
     for (int r = 0; r < ti.rows; r += 16) {
       TileInfo part = ti;
       part.row0 = ti.row0 + r;
       part.rows = min(16, ti.rows - r);
-      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, rot, ti.rows <= 16, ring);
+      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, rot, ti.rows <= 16, tok, r, ring);
     }
   } else if constexpr (kSkinnyTwoBlocks) {
     // 32 rows per pass
@@ -220,7 +343,7 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
       TileInfo part = ti;
       part.row0 = ti.row0 + r;
       part.rows = min(32, ti.rows - r);
-      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, rot, ti.rows <= 32, ring);
+      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, rot, ti.rows <= 32, tok, r, ring);
     }
   }
 }
