@@ -80,9 +80,11 @@ template <> struct Oct<bf16_t> {
 
 constexpr int kWaves = 8;
 
-// value of the lane n places further round this lane's 16-lane row (DPP row_ror)
+// value of the lane n places further round this lane's 16-lane row (DPP row_ror;
+// a rotation never leaves the row, so bound_ctrl never applies and no "old"
+// value has to be set up)
 template <int n> __device__ __forceinline__ int row_ror(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, 0x120 + n, 0xF, 0xF, false);
+  return __builtin_amdgcn_mov_dpp(v, 0x120 + n, 0xF, 0xF, true);
 }
 template <int n> __device__ __forceinline__ float row_ror(float v) {
   return __int_as_float(row_ror<n>(__float_as_int(v)));
@@ -110,22 +112,22 @@ __device__ __forceinline__ float key_logit(uint64_t key) {
 }
 __device__ __forceinline__ int key_expert(uint64_t key) { return static_cast<int>(~static_cast<uint32_t>(key)); }
 
-template <int n> __device__ __forceinline__ uint64_t row_ror64(uint64_t v) {
-  const uint32_t lo = static_cast<uint32_t>(row_ror<n>(static_cast<int>(static_cast<uint32_t>(v))));
-  const uint32_t hi = static_cast<uint32_t>(row_ror<n>(static_cast<int>(static_cast<uint32_t>(v >> 32))));
-  return (static_cast<uint64_t>(hi) << 32) | lo;
-}
-
-// maximum over the 16-lane row, in every lane
+// maximum over the 16-lane row, in every lane: the maximum high word, then the
+// maximum low word among the lanes holding it (the same key as a 64-bit
+// maximum; a valid key's low word ~expert is never 0)
 __device__ __forceinline__ uint64_t row_max64(uint64_t v) {
-  uint64_t o = row_ror64<8>(v);
-  v = o > v ? o : v;
-  o = row_ror64<4>(v);
-  v = o > v ? o : v;
-  o = row_ror64<2>(v);
-  v = o > v ? o : v;
-  o = row_ror64<1>(v);
-  return o > v ? o : v;
+  const uint32_t hi = static_cast<uint32_t>(v >> 32), lo = static_cast<uint32_t>(v);
+  uint32_t m = hi;
+  m = max(m, static_cast<uint32_t>(row_ror<8>(static_cast<int>(m))));
+  m = max(m, static_cast<uint32_t>(row_ror<4>(static_cast<int>(m))));
+  m = max(m, static_cast<uint32_t>(row_ror<2>(static_cast<int>(m))));
+  m = max(m, static_cast<uint32_t>(row_ror<1>(static_cast<int>(m))));
+  uint32_t l = hi == m ? lo : 0u;
+  l = max(l, static_cast<uint32_t>(row_ror<8>(static_cast<int>(l))));
+  l = max(l, static_cast<uint32_t>(row_ror<4>(static_cast<int>(l))));
+  l = max(l, static_cast<uint32_t>(row_ror<2>(static_cast<int>(l))));
+  l = max(l, static_cast<uint32_t>(row_ror<1>(static_cast<int>(l))));
+  return (static_cast<uint64_t>(m) << 32) | l;
 }
 
 // bitonic sort, descending, of n (a power of two) keys in registers
@@ -566,8 +568,9 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
     // k rounds: the row maximum of the lanes' heads is the next slot; the lane
     // that held it pops its head
     uint64_t mykey = 0, topkey = 0;
-#pragma unroll 1
-    for (int i = 0; i < k; ++i) {
+#pragma unroll
+    for (int i = 0; i < kMaxK; ++i) {
+      if (i >= k) break;
       const uint64_t m = row_max64(head[0]);
       if (i == 0) topkey = m;
       if (sub == i) mykey = m;
