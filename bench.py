@@ -64,6 +64,9 @@ def parse():
     ap.add_argument("--decode-only", action="store_true",
                     help="time only the decode batches (prints their JSON, not the prefill contract line)")
     ap.add_argument("--decode-batches", default="1,8,32,64", help="comma-separated decode batch sizes")
+    ap.add_argument("--ace-only", action="store_true",
+                    help="decode legs: time only the ACE layer (no plain top-k layer, no graph replays), "
+                         "so per-dispatch counters of a profiler run belong to it alone")
     ap.add_argument("--zipf-only", action="store_true",
                     help="time only the 256-expert Zipf workload (prints its JSON, not the contract line)")
     ap.add_argument("--stack", action="store_true",
@@ -440,21 +443,22 @@ def main():
         for B in [int(b) for b in args.decode_batches.split(",") if b]:
             xb = torch.from_numpy(synth.decode_inputs(cfg.with_(T=B), B, step=0)).to(dev).to(bf)
             s_ace, o_ace = make_step(xb, False, tau)
-            s_top, _ = make_step(xb, True, tau)
             ms_a = time_steps(s_ace, max(args.steps, 50), args.warmup, torch)
-            ms_t = time_steps(s_top, max(args.steps, 50), args.warmup, torch)
-            ms_ga, ms_gt = graph_ms(s_ace, max(args.steps, 50)), graph_ms(s_top, max(args.steps, 50))
             kb = o_ace["keep"].cpu().numpy()
             ea = int((o_ace["counts"].cpu().numpy() > 0).sum())
             bb, _ = layer_bytes(B, d, N, k, m, ea, int(kb.sum()))
-            dec[str(B)] = {"tokens_per_s": round(B / (ms_a * 1e-3), 1), "ms_per_step": round(ms_a, 4),
-                           "topk_ms_per_step": round(ms_t, 4), "speedup_vs_topk": round(ms_t / ms_a, 4),
-                           "graph_ms_per_step": round(ms_ga, 4), "graph_topk_ms_per_step": round(ms_gt, 4),
-                           "graph_tokens_per_s": round(B / (ms_ga * 1e-3), 1),
-                           "graph_speedup_vs_topk": round(ms_gt / ms_ga, 4),
-                           "realised_skip": round(float(1 - kb.mean()), 4), "experts_active": ea,
-                           "alg_gbs": round(bb / (ms_a * 1e-3) / 1e9, 1),
-                           "hbm_frac": round(bb / (ms_a * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+            dec[str(B)] = {"tokens_per_s": round(B / (ms_a * 1e-3), 1), "ms_per_step": round(ms_a, 4)}
+            if not args.ace_only:
+                s_top, _ = make_step(xb, True, tau)
+                ms_t = time_steps(s_top, max(args.steps, 50), args.warmup, torch)
+                ms_ga, ms_gt = graph_ms(s_ace, max(args.steps, 50)), graph_ms(s_top, max(args.steps, 50))
+                dec[str(B)].update({"topk_ms_per_step": round(ms_t, 4), "speedup_vs_topk": round(ms_t / ms_a, 4),
+                                    "graph_ms_per_step": round(ms_ga, 4), "graph_topk_ms_per_step": round(ms_gt, 4),
+                                    "graph_tokens_per_s": round(B / (ms_ga * 1e-3), 1),
+                                    "graph_speedup_vs_topk": round(ms_gt / ms_ga, 4)})
+            dec[str(B)].update({"realised_skip": round(float(1 - kb.mean()), 4), "experts_active": ea,
+                                "alg_bytes": int(bb), "alg_gbs": round(bb / (ms_a * 1e-3) / 1e9, 1),
+                                "hbm_frac": round(bb / (ms_a * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)})
             log(f"decode B={B}: {dec[str(B)]}")
         return dec
 
