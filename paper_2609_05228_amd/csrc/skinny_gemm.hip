@@ -7,14 +7,17 @@
 //    LDS ring with global_load_lds_dwordx4, one 8-row x 128-byte unit per
 //    instruction (whole cache lines; see lds_dma.h; weights carry the
 //    non-temporal hint when the wave makes one pass over them), P stages of 64 k
-//    deep, and
-//    waits only on its own vmcnt: no barriers, waves run independently;
+//    deep, and waits only on its own vmcnt: no barriers, waves run independently;
 //  * it reads MFMA fragments back from the ring and multiplies them with
 //    v_mfma_f32_16x16x32_bf16;
 //  * with one K split the epilogue writes H (SwiGLU applied) or Y in bf16;
 //    with several, it writes fp32 partial sums, which swiglu_reduce_kernel (for
 //    H) and the combine kernel (for Y) add in split order, so the result does
-//    not depend on scheduling.
+//    not depend on scheduling;
+//  * batches of 2-4 router chunks need no plan kernel: each gate/up wave derives
+//    its tile and the tokens of its rows from the router's per-chunk counts and
+//    the routing (self_tile), and the gate/up launch writes the plan outputs and
+//    the tile list for the down launch.
 #include "lds_dma.h"
 
 namespace ace {
