@@ -57,6 +57,7 @@ constexpr int kMaxK = 8;     // top-k supported by the router kernel
 constexpr int kTileM = 256;  // rows of one grouped-GEMM M tile (the dispatch plan's tile size)
 constexpr int kRouteTokens = 16;  // tokens per router workgroup (one dispatch-plan chunk)
 constexpr int kRouteMaxSlices = 16;  // K slices of the small-batch router
+constexpr int kRoutePairMinChunks = 256;  // bf16 batches of more chunks: one router workgroup per chunk pair
 constexpr int kRouteMaxSplitChunks = 16;  // most chunks that take the small-batch (K-slice) router path
 
 // 16-expert tiles the router kernels are compiled for: 1, 2, 4, 8 or 16 (>= N / 16)

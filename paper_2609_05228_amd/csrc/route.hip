@@ -418,6 +418,93 @@ __device__ __forceinline__ void plan_one_chunk(const RouteArgs &a, const uint32_
 // NT = number of 16-expert tiles covered (N <= 16 * NT).  SPLIT: the logits
 // come from route_partial_kernel's K slices; otherwise the 8 waves compute
 // them here over all of K.
+// Top-k, gates and Alg. 4 for token t (valid if tvalid) held by one 16-lane
+// group, lane `sub` holding slot `sub` (sub < k); zrow = the token's N logits
+// in LDS.  Writes the token's routing outputs; returns the expert and keep
+// decision of this lane's slot through my_e / my_kept.
+template <int NT>
+__device__ __forceinline__ void select_token(const RouteArgs &a, const float *zrow, int t, bool tvalid, int sub,
+                                             const float *a_gsp_s, const float *a_rcr_s, int &my_e, bool &my_kept) {
+  const int N = a.N;
+  const int k = a.k;
+  // this lane's candidates, experts sub + 16 q, sorted; it can lose at most k <= 8 of them
+  uint64_t cand[NT];
+#pragma unroll
+  for (int q = 0; q < NT; ++q) {
+    const int e = sub + 16 * q;
+    cand[q] = (e < N) ? topk_key(zrow[e], e) : 0ull;
+  }
+  sort_desc<NT>(cand);
+  constexpr int L = NT < kMaxK ? NT : kMaxK;
+  uint64_t head[L];
+#pragma unroll
+  for (int q = 0; q < L; ++q) head[q] = cand[q];
+  // k rounds: the row maximum of the lanes' heads is the next slot; the lane
+  // that held it pops its head
+  uint64_t mykey = 0, topkey = 0;
+#pragma unroll
+  for (int i = 0; i < kMaxK; ++i) {
+    if (i >= k) break;
+    const uint64_t m = row_max64(head[0]);
+    if (i == 0) topkey = m;
+    if (sub == i) mykey = m;
+    const bool win = head[0] == m;
+#pragma unroll
+    for (int q = 0; q + 1 < L; ++q) head[q] = win ? head[q + 1] : head[q];
+    head[L - 1] = win ? 0ull : head[L - 1];
+  }
+  const bool slot = sub < k;
+  const int se = slot ? key_expert(mykey) : 0;  // this lane's slot: expert and logit
+  const float sz = key_logit(mykey), ztop = key_logit(topkey);
+  // renormalised top-k gate
+  const float ge = slot ? expf(sz - ztop) : 0.f;
+  const float g = ge / group_sum(ge);
+  // Alg. 4: s = g * A(e); p = s / (sum s + eps); ACE: c = max(p_GSP, p_RCR)
+  const float sg = slot ? g * a_gsp_s[se] : 0.f;
+  const float sr = slot ? g * a_rcr_s[se] : 0.f;
+  const float pg = sg / (group_sum(sg) + a.eps);
+  const float pr = sr / (group_sum(sr) + a.eps);
+  float c;
+  switch (a.fusion) {
+    case 1: c = fminf(pg, pr); break;           // either view low (union)
+    case 2: c = (pg + pr) * 0.5f; break;        // mean of the views
+    case 3: c = pg; break;                      // GSP only
+    case 4: c = pr; break;                      // RCR only
+    case 5: {                                   // router score: the p of a table of ones
+      const float gs = slot ? g : 0.f;
+      c = gs / (group_sum(gs) + a.eps);
+      break;
+    }
+    default: c = fmaxf(pg, pr);                 // ACE: both views low (intersection)
+  }
+  // slot 0 is the top-1 expert, never skipped
+  const bool skip = !a.skip_disable && sub > 0 && c < a.tau;
+  bool kept = slot && !skip;
+  const int nkept = group_count(kept);
+  if (!a.skip_disable && nkept < a.m_min) {
+    // restore skipped slots by descending c (ties -> lower slot) up to m_min
+    int rank = 0;
+#pragma unroll 1
+    for (int jj = 0; jj < k; ++jj) {
+      const float cj = __shfl(c, jj, 16);
+      const int kj = __shfl(kept ? 1 : 0, jj, 16);
+      if (!kj && jj != sub && (cj > c || (cj == c && jj < sub))) ++rank;
+    }
+    kept = kept || (slot && rank < a.m_min - nkept);
+  }
+  const float zgate = group_sum(kept ? g : 0.f) + a.eps;
+  if (tvalid && slot) {
+    const size_t o = static_cast<size_t>(t) * k + sub;
+    a.topk_idx[o] = se;
+    a.keep[o] = kept ? 1 : 0;
+    a.gates[o] = a.skip_disable ? g : (kept ? g / zgate : 0.f);
+    if (a.scores) a.scores[o] = c;
+    if (!kept) a.slot_row[o] = -1;
+    my_e = se;
+    my_kept = kept;
+  }
+}
+
 template <typename T, int NT, bool SPLIT>
 __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   constexpr int NP = NT * 16;
@@ -550,85 +637,7 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   } else {
     // ---- 2. top-k, gates and Alg. 4 (waves 0-3): one token per 16-lane
     // group, lane `sub` holds slot `sub` (sub < k)
-    const int k = a.k;
-    const bool tvalid = t < nt;
-    const float *zrow = zred[0][tl];
-    // this lane's candidates, experts sub + 16 q, sorted; it can lose at most k <= 8 of them
-    uint64_t cand[NT];
-#pragma unroll
-    for (int q = 0; q < NT; ++q) {
-      const int e = sub + 16 * q;
-      cand[q] = (e < N) ? topk_key(zrow[e], e) : 0ull;
-    }
-    sort_desc<NT>(cand);
-    constexpr int L = NT < kMaxK ? NT : kMaxK;
-    uint64_t head[L];
-#pragma unroll
-    for (int q = 0; q < L; ++q) head[q] = cand[q];
-    // k rounds: the row maximum of the lanes' heads is the next slot; the lane
-    // that held it pops its head
-    uint64_t mykey = 0, topkey = 0;
-#pragma unroll
-    for (int i = 0; i < kMaxK; ++i) {
-      if (i >= k) break;
-      const uint64_t m = row_max64(head[0]);
-      if (i == 0) topkey = m;
-      if (sub == i) mykey = m;
-      const bool win = head[0] == m;
-#pragma unroll
-      for (int q = 0; q + 1 < L; ++q) head[q] = win ? head[q + 1] : head[q];
-      head[L - 1] = win ? 0ull : head[L - 1];
-    }
-    const bool slot = sub < k;
-    const int se = slot ? key_expert(mykey) : 0;  // this lane's slot: expert and logit
-    const float sz = key_logit(mykey), ztop = key_logit(topkey);
-    // renormalised top-k gate
-    const float ge = slot ? expf(sz - ztop) : 0.f;
-    const float g = ge / group_sum(ge);
-    // Alg. 4: s = g * A(e); p = s / (sum s + eps); ACE: c = max(p_GSP, p_RCR)
-    const float sg = slot ? g * a_gsp_s[se] : 0.f;
-    const float sr = slot ? g * a_rcr_s[se] : 0.f;
-    const float pg = sg / (group_sum(sg) + a.eps);
-    const float pr = sr / (group_sum(sr) + a.eps);
-    float c;
-    switch (a.fusion) {
-      case 1: c = fminf(pg, pr); break;           // either view low (union)
-      case 2: c = (pg + pr) * 0.5f; break;        // mean of the views
-      case 3: c = pg; break;                      // GSP only
-      case 4: c = pr; break;                      // RCR only
-      case 5: {                                   // router score: the p of a table of ones
-        const float gs = slot ? g : 0.f;
-        c = gs / (group_sum(gs) + a.eps);
-        break;
-      }
-      default: c = fmaxf(pg, pr);                 // ACE: both views low (intersection)
-    }
-    // slot 0 is the top-1 expert, never skipped
-    const bool skip = !a.skip_disable && sub > 0 && c < a.tau;
-    bool kept = slot && !skip;
-    const int nkept = group_count(kept);
-    if (!a.skip_disable && nkept < a.m_min) {
-      // restore skipped slots by descending c (ties -> lower slot) up to m_min
-      int rank = 0;
-#pragma unroll 1
-      for (int jj = 0; jj < k; ++jj) {
-        const float cj = __shfl(c, jj, 16);
-        const int kj = __shfl(kept ? 1 : 0, jj, 16);
-        if (!kj && jj != sub && (cj > c || (cj == c && jj < sub))) ++rank;
-      }
-      kept = kept || (slot && rank < a.m_min - nkept);
-    }
-    const float zgate = group_sum(kept ? g : 0.f) + a.eps;
-    if (tvalid && slot) {
-      const size_t o = static_cast<size_t>(t) * k + sub;
-      a.topk_idx[o] = se;
-      a.keep[o] = kept ? 1 : 0;
-      a.gates[o] = a.skip_disable ? g : (kept ? g / zgate : 0.f);
-      if (a.scores) a.scores[o] = c;
-      if (!kept) a.slot_row[o] = -1;
-      my_e = se;
-      my_kept = kept;
-    }
+    select_token<NT>(a, zred[0][tl], t, t < nt, sub, a_gsp_s, a_rcr_s, my_e, my_kept);
   }
   // ---- per-expert token masks of this chunk -> local ranks and counts
   if (my_kept) atomicOr(&emask[my_e], 1u << tl);
@@ -645,9 +654,225 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
     a.chunk_count[static_cast<size_t>(blockIdx.x) * N + e] = static_cast<uint8_t>(__popc(emask[e]));
 }
 
+// Batches of more than 256 chunks (bf16): one workgroup of 8 waves per pair of
+// chunks (32 tokens).  Each router-row fragment a wave loads feeds the MFMAs of
+// both 16-token tiles, so every CU streams W_r once per two chunks, and the
+// grid is one round of workgroups instead of two.  Same products and the same
+// kind of fixed summation as route_kernel (blocks in order within a wave; then
+// waves w and w + 4 first, those four sums in order); then selection (waves
+// 0-3: the first chunk's tokens, waves 4-7: the second's), x_in for the 32
+// rows, and per-chunk ranks and counts.
+constexpr int kPairWaves = 8;
+template <int NT> struct PairStage {
+  uint4 x[2], g, w[NT];
+};
+// K blocks in flight per wave within 2 waves per SIMD: accumulators 8 NT, a stage
+// 4 (3 + NT), about 40 more
+template <int NT> struct PairDepth {
+  static constexpr int fit = (256 - 8 * NT - 40) / ((3 + NT) * 4);
+  static constexpr int value = fit >= 3 ? 3 : fit >= 1 ? fit : 1;
+};
+
+template <int NT>
+__global__ __launch_bounds__(512) void route_pair_kernel(RouteArgs a) {
+  constexpr int NP = NT * 16, TOK = 2 * kTok;
+  constexpr int D = PairDepth<NT>::value;
+  static_assert(512 % NP == 0, "a thread meets one expert column in the logits reduction");
+  __shared__ float zred[kPairWaves / 2][TOK][NP + 1];  // waves w and w + 4 share slot w
+  __shared__ float ssred[kPairWaves][TOK];
+  __shared__ float rstd_s[TOK];
+  __shared__ uint32_t emask[2][NP];
+  __shared__ float a_gsp_s[NP], a_rcr_s[NP];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, grp = lane >> 4;
+  const int t0 = blockIdx.x * TOK;
+  const int d = a.d, N = a.N, nt = a.T;
+  const int G = (nt + kTok - 1) / kTok;
+  const bf16_t *x = static_cast<const bf16_t *>(a.x);
+  const bf16_t *gamma = static_cast<const bf16_t *>(a.gamma);
+  bf16_t *xn = static_cast<bf16_t *>(a.xn);
+  if (tid < NP) {
+    emask[0][tid] = emask[1][tid] = 0u;
+    a_gsp_s[tid] = tid < N ? a.a_gsp[tid] : 0.f;
+    a_rcr_s[tid] = tid < N ? a.a_rcr[tid] : 0.f;
+  }
+  const float bias = (a.b_router && (tid % NP) < N) ? a.b_router[tid % NP] : 0.f;
+
+  // ---- 1. logits of both token tiles: wave w takes K blocks w, w + 4, ...
+  {
+    const int lrow = lane >> 2, lchunk = lane & 3;  // row-major fragment loads
+    const bf16_t *xrow[2];
+#pragma unroll
+    for (int c = 0; c < 2; ++c) xrow[c] = x + static_cast<size_t>(min(t0 + 16 * c + lrow, nt - 1)) * d + lchunk * 8;
+    const bf16_t *gl = gamma + grp * 8;
+    const bf16_t *wl = static_cast<const bf16_t *>(a.w_router) + lchunk * 8;
+    int woff[NT];
+#pragma unroll
+    for (int f = 0; f < NT; ++f) woff[f] = min(16 * f + lrow, N - 1) * d;
+    f32x4_t acc[2][NT];
+    float ss[2] = {0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int f = 0; f < NT; ++f) acc[c][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int nb = d >> 5;
+    const int cnt = nb > wave ? (nb - wave + kPairWaves - 1) / kPairWaves : 0;
+    const int rot = cnt > 0 ? static_cast<int>((blockIdx.x >> 3) % cnt) : 0;
+    for (int i0 = 0; i0 < cnt; i0 += D) {
+      PairStage<NT> st[D];
+#pragma unroll
+      for (int u = 0; u < D; ++u) {
+        if (u > 0 && i0 + u >= cnt) break;
+        int i = i0 + u + rot;
+        i = i >= cnt ? i - cnt : i;
+        const int k = 32 * (wave + i * kPairWaves);
+#pragma unroll
+        for (int c = 0; c < 2; ++c) st[u].x[c] = *reinterpret_cast<const uint4 *>(xrow[c] + k);
+        st[u].g = *reinterpret_cast<const uint4 *>(gl + k);
+#pragma unroll
+        for (int f = 0; f < NT; ++f) st[u].w[f] = *reinterpret_cast<const uint4 *>(wl + woff[f] + k);
+      }
+#pragma unroll
+      for (int u = 0; u < D; ++u) {
+        if (u > 0 && i0 + u >= cnt) break;
+        float gv[8];
+        Oct<bf16_t>::cvt(st[u].g, gv);
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+          float xv[8];
+          Oct<bf16_t>::cvt(to_operand_order(st[u].x[c]), xv);
+          uint32_t hi[4], lo[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            uint32_t h[2], l[2];
+#pragma unroll
+            for (int v = 0; v < 2; ++v) {
+              const float xe = xv[2 * q + v];
+              ss[c] = fmaf(xe, xe, ss[c]);
+              const float pr = xe * gv[2 * q + v];  // exact: two 8-bit significands
+              const uint32_t pb = __float_as_uint(pr) & 0xFFFF0000u;
+              h[v] = pb;
+              l[v] = __float_as_uint(pr - __uint_as_float(pb));  // exact, <= 8 significant bits
+            }
+            hi[q] = (h[0] >> 16) | h[1];
+            lo[q] = (l[0] >> 16) | (l[1] & 0xFFFF0000u);
+          }
+          const bf16x8_t ahi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+          const bf16x8_t alo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+#pragma unroll
+          for (int f = 0; f < NT; ++f) {
+            const bf16x8_t w = __builtin_bit_cast(bf16x8_t, to_operand_order(st[u].w[f]));
+            acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, w, acc[c][f], 0, 0, 0);
+            acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, w, acc[c][f], 0, 0, 0);
+          }
+        }
+      }
+    }
+    // D[row = token 4 grp + i][col = expert 16 f + r16] of each token tile:
+    // waves 0-3 store theirs, then waves 4-7 add theirs to slot wave - 4
+    const int slot = wave & 3;
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      float v = ss[c];
+      v += __shfl_xor(v, 16);
+      v += __shfl_xor(v, 32);
+      if (grp == 0) ssred[wave][16 * c + r16] = v;
+    }
+    if (wave < 4) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int f = 0; f < NT; ++f)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) zred[slot][16 * c + grp * 4 + i][16 * f + r16] = acc[c][f][i];
+    }
+    __syncthreads();
+    if (wave >= 4) {
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+#pragma unroll
+        for (int f = 0; f < NT; ++f)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) zred[slot][16 * c + grp * 4 + i][16 * f + r16] += acc[c][f][i];
+    }
+  }
+  __syncthreads();
+  if (tid < TOK) {
+    float ssum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kPairWaves; ++w) ssum += ssred[w][tid];
+    rstd_s[tid] = 1.0f / sqrtf(ssum / static_cast<float>(d) + a.rms_eps);
+  }
+  __syncthreads();
+  for (int idx = tid; idx < TOK * NP; idx += 512) {
+    const int tl = idx / NP;
+    const int e = idx - tl * NP;
+    float z = 0.f;
+#pragma unroll
+    for (int w = 0; w < kPairWaves / 2; ++w) z += zred[w][tl][e];
+    zred[0][tl][e] = z * rstd_s[tl] + bias;
+  }
+  __syncthreads();
+
+  // ---- 2. selection: waves 0-3 the first chunk's tokens, waves 4-7 the second's,
+  // one token per 16-lane group
+  const int sub = lane & 15;
+  const int p = wave >> 2;                        // this wave's chunk
+  const int tlc = (wave & 3) * 4 + (lane >> 4);   // token within its chunk
+  int my_e = -1;
+  bool my_kept = false;
+  {
+    const int t = t0 + 16 * p + tlc;
+    select_token<NT>(a, zred[0][16 * p + tlc], t, t < nt, sub, a_gsp_s, a_rcr_s, my_e, my_kept);
+  }
+  // ---- 3. x_in = x * rstd * gamma for the expert GEMMs, 16 rows at a time
+  const int d8 = d >> 3;
+  for (int c8 = tid; c8 < 2 * d8; c8 += 512) {
+    // thread pairs (c8, c8 + d8) share a column octet: rows of chunk q = c8 / d8
+    const int q = c8 >= d8 ? 1 : 0, o8 = c8 - q * d8;
+    float gv[8];
+    Oct<bf16_t>::cvt(Oct<bf16_t>::load(gamma + 8 * o8), gv);
+    {
+      const int r0 = t0 + 16 * q;
+      typename Oct<bf16_t>::raw xr[kTok];
+#pragma unroll
+      for (int u = 0; u < kTok; ++u) xr[u] = Oct<bf16_t>::load(x + static_cast<size_t>(min(r0 + u, nt - 1)) * d + 8 * o8);
+#pragma unroll
+      for (int u = 0; u < kTok; ++u) {
+        if (r0 + u >= nt) break;
+        float xv[8], av[8];
+        Oct<bf16_t>::cvt(xr[u], xv);
+        const float rs = rstd_s[16 * q + u];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) av[i] = (xv[i] * rs) * gv[i];
+        Oct<bf16_t>::store(xn + static_cast<size_t>(r0 + u) * d + 8 * o8, av);
+      }
+    }
+  }
+  // ---- 4. per-expert token masks of each chunk -> local ranks and counts
+  if (my_kept) atomicOr(&emask[p][my_e], 1u << tlc);
+  __syncthreads();
+  if (my_kept) {
+    const int t = t0 + 16 * p + tlc;
+    a.local_rank[static_cast<size_t>(t) * a.k + sub] = static_cast<uint8_t>(__popc(emask[p][my_e] & ((1u << tlc) - 1u)));
+  }
+  for (int i = tid; i < 2 * N; i += 512) {
+    const int q = i >= N ? 1 : 0, e = i - q * N;
+    const int c = 2 * blockIdx.x + q;
+    if (c < G) a.chunk_count[static_cast<size_t>(c) * N + e] = static_cast<uint8_t>(__popc(emask[q][e]));
+  }
+}
+
 template <typename T, int NT>
 void launch_route_nt(const RouteArgs &a, hipStream_t stream) {
   const int chunks = (a.T + kTok - 1) / kTok;
+  if constexpr (sizeof(T) == 2) {
+    if (a.ksplit == 0 && chunks > kRoutePairMinChunks) {
+      route_pair_kernel<NT><<<dim3((chunks + 1) / 2), 512, 0, stream>>>(a);
+      return;
+    }
+  }
   if (a.ksplit > 0) {
     route_partial_kernel<T, NT><<<dim3(chunks, a.ksplit), 256, 0, stream>>>(a);
     route_kernel<T, NT, true><<<dim3(chunks), 512, 0, stream>>>(a);
