@@ -19,7 +19,8 @@
 //     skip decisions never see bf16-rounded activations.
 //     A CU keeps only a few tens of KB of loads in flight, so one workgroup
 //     reading all of W_r is latency-bound.  Large batches (> 16 chunks) run one
-//     fused workgroup of 8 waves per chunk (every CU busy anyway); small
+//     fused workgroup of 8 waves per chunk (every CU busy anyway; above 256
+//     chunks in bf16, one per chunk pair, route_pair_kernel); small
 //     batches first spread W_r over (chunk, K slice) workgroups that write
 //     partial logits, and the per-chunk kernel adds the slices.
 //  2. Selection (waves 0-3, one token per 16-lane group, lane i holds slot i):
