@@ -351,7 +351,11 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
   }
 }
 
-// H = SiLU(sum_s gate partials) * (sum_s up partials), splits added in order
+constexpr int kMaxGateUpSplits = 8;  // K splits of the small-batch gate/up GEMM
+
+// H = SiLU(sum_s gate partials) * (sum_s up partials), splits added in order.
+// All splits' partials are loaded before the first add, so the L2 round trips
+// overlap instead of following one another; the sums keep split order.
 __global__ __launch_bounds__(256) void swiglu_reduce_kernel(SkinnyArgs sa, const int32_t *n_rows) {
   const GemmArgs &a = sa.g;
   const int rows = a.dense_rows > 0 ? a.dense_rows : n_rows[0];
@@ -360,10 +364,19 @@ __global__ __launch_bounds__(256) void swiglu_reduce_kernel(SkinnyArgs sa, const
   const size_t plane = static_cast<size_t>(sa.rows_cap) * a.m;
   for (size_t i = blockIdx.x * static_cast<size_t>(blockDim.x) + threadIdx.x; i < total;
        i += static_cast<size_t>(gridDim.x) * blockDim.x) {
+    float pg[kMaxGateUpSplits], pu[kMaxGateUpSplits];
+#pragma unroll
+    for (int s = 0; s < kMaxGateUpSplits; ++s)
+      if (s < sa.splits) {
+        pg[s] = sa.part0[s * plane + i];
+        pu[s] = sa.part1[s * plane + i];
+      }
     float gs = 0.f, us = 0.f;
-    for (int s = 0; s < sa.splits; ++s) {
-      gs += sa.part0[s * plane + i];
-      us += sa.part1[s * plane + i];
+#pragma unroll
+    for (int s = 0; s < kMaxGateUpSplits; ++s) {
+      if (s >= sa.splits) break;
+      gs += pg[s];
+      us += pu[s];
     }
     H[i] = f32_to_bf16(silu_for_bf16(gs) * us);
   }
@@ -378,6 +391,7 @@ hipError_t launch_skinny(const SkinnyArgs &sa, bool gateup, const int32_t *n_row
   const long items = static_cast<long>(a.max_groups) * sa.splits * nN;
   const dim3 grid(static_cast<unsigned>((items + kSkinnyWavesPerGroup - 1) / kSkinnyWavesPerGroup));
   if (gateup) {
+    if (sa.splits > kMaxGateUpSplits) return hipErrorInvalidValue;
     skinny_gemm_kernel<true><<<grid, kSkinnyWavesPerGroup * 64, 0, stream>>>(sa);
     if (sa.splits > 1) {
       const size_t total = static_cast<size_t>(sa.rows_cap) * a.m;
