@@ -417,8 +417,9 @@ def main():
         log(f"calibration copy of {args.calib_copy_mb} MiB done")
         del src, dst
 
-    def graph_ms(fn, steps):
-        """ms per step of `fn` captured once in a HIP graph and replayed (no host launch cost)."""
+    def graph_ms(fn, steps, calls=10):
+        """ms per call of `fn`, `calls` calls captured in one HIP graph and replayed: the
+        host cost of one graph launch is spread over `calls` layer calls."""
         side = torch.cuda.Stream()
         side.wait_stream(torch.cuda.current_stream())
         with torch.cuda.stream(side):
@@ -427,15 +428,17 @@ def main():
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
-            fn()
+            for _ in range(calls):
+                fn()
         for _ in range(3):
             g.replay()
         torch.cuda.synchronize()
+        reps = max(1, steps // calls)
         t = time.perf_counter()
-        for _ in range(steps):
+        for _ in range(reps):
             g.replay()
         torch.cuda.synchronize()
-        return (time.perf_counter() - t) / steps * 1e3
+        return (time.perf_counter() - t) / (reps * calls) * 1e3
 
     def decode_legs():
         """Decode batches through the same layer, tau transferred from prefill."""
