@@ -18,8 +18,9 @@ Modules
            taken inside the 1e-6 tie band.
 
 Pinning status: every function is pinned by `tests/test_oracle_*.py` against
-closed forms, invariants the paper proves, brute force on tiny inputs, or the
-hand-derived Alg. 4 worked example in `tests/golden/`.  The absolute values
+closed forms, invariants the paper proves, brute force on tiny inputs, the
+hand-derived Alg. 4 worked example in `tests/golden/`, or (the tie checker)
+hand-built tokens with known margins and known admissible decisions.  The absolute values
 of the GSP/RCR tables for the paper's real models are parity unpinned (the
 paper prints none); only their structural properties are pinned.
 """

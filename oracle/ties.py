@@ -74,17 +74,20 @@ def admissible_token(z_row, pi_row, gpu_idx_row, gpu_keep_row, a_gsp, a_rcr, tau
     g = top / top.sum()
     c = _alg4_scores(g, np.asarray(a_gsp, np.float64)[idx], np.asarray(a_rcr, np.float64)[idx], eps, fusion)
     skip_final = {i for i in range(1, k) if not keep[i]}
-    clear_skip = {i for i in range(1, k) if c[i] < tau - band}
+    # every non-top-1 slot is exactly one of: ambiguous (|c - tau| inside the band),
+    # clearly skippable (c < tau outside the band) or clearly kept (c >= tau outside it)
     ambiguous = [i for i in range(1, k) if abs(c[i] - tau) < band]
+    clear_skip = {i for i in range(1, k) if c[i] < tau and i not in ambiguous}
     for r in range(len(ambiguous) + 1):
         for extra in combinations(ambiguous, r):
-            s0 = clear_skip | set(extra)
-            need = max(0, m_min - (k - len(s0)))
+            s0 = clear_skip | set(extra)            # one resolution of the strict c < tau tests
+            need = max(0, m_min - (k - len(s0)))    # slots the m_min safeguard restores
             if not skip_final <= s0:
                 continue
             restored = s0 - skip_final
             if len(restored) != need:
                 continue
+            # restore order: descending c, so no final skip may clearly beat a restored slot
             if all(c[a] >= c[b] - band for a in restored for b in skip_final):
                 return True, "ok"
     return False, "keep mask not reachable from any near-tie resolution"

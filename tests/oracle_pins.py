@@ -481,4 +481,157 @@ def check_plan():
     assert p["slot_row"].tolist() == [[4, 0], [1, -1], [5, 2], [3, -1]]
 
 
+# --------------------------------------------------------------------------- tie accounting
+# Hand-built tokens for each decision margin the parity tests excuse (the benchmark spec: ties
+# within 1e-6 are counted): the top-k boundary and the in-top-k slot order (Sec. 3.1,
+# ties to the lower id), the strict c < tau test of a non-top-1 slot (Alg. 4, top-1
+# kept) and, with m_min > 1, the restore order by descending c (Alg. 4).  Logits and
+# contributions are written out here with plain numpy, not taken from the oracle.
+_TB = 1e-6  # the tie band
+
+
+def _tok(z, idx, a=None, eps=1e-6):
+    """pi, gates and contributions c of one hand-built token whose experts `idx`
+    (slot order) are routed; a = the per-expert table used for both views
+    (so p_GSP = p_RCR = c), all ones by default."""
+    z = np.asarray(z, float)
+    e = np.exp(z - z.max())
+    pi = e / e.sum()
+    g = pi[idx] / pi[idx].sum()
+    a = np.ones(z.size) if a is None else np.asarray(a, float)
+    s = g * a[idx]
+    return pi, g, s / (s.sum() + eps)
+
+
+def check_ties_margins_hand_tokens():
+    T = oracle.ties
+    inf = np.inf
+    # (a) k-th and (k+1)-th logits 4e-7 apart: the top-k set is ambiguous
+    m = T.token_margins([3.0, 1.0 + 4e-7, 1.0, 0.0, -1.0], [0, 1], [0.7, 0.3], inf, 1)
+    assert abs(m["boundary"] - 4e-7) < 1e-12 and abs(m["order"] - (2.0 - 4e-7)) < 1e-12, m
+    assert T.is_tied(m, _TB)
+    # the same token one logit further: nothing tied (boundary is z_(k) - z_(k+1), not z_(k+1) - z_(k+2))
+    m = T.token_margins([3.0, 1.0 + 4e-7, 1.0, 0.0, -1.0], [0, 1, 2], [0.6, 0.3, 0.1], inf, 1)
+    assert abs(m["boundary"] - 1.0) < 1e-12 and abs(m["order"] - 4e-7) < 1e-12, m
+    assert T.is_tied(m, _TB)                               # via the order of slots 1 and 2
+    m = T.token_margins([3.0, 1.0 + 4e-7, 1.0 - 1e-3, 0.0, 0.0 - 2e-7], [0, 1, 2], [0.6, 0.3, 0.1], inf, 1)
+    assert abs(m["boundary"] - (1.0 - 1e-3)) < 1e-12 and not T.is_tied(m, _TB), m
+    # (b) order: the margin is taken along the slot order (descending logits), whatever the ids
+    m = T.token_margins([0.0, 3.0, 1.0, 2.0, -1.0], [1, 3, 2], [0.6, 0.3, 0.1], inf, 1)
+    assert m["order"] == 1.0 and m["boundary"] == 1.0 and not T.is_tied(m, _TB), m
+    m = T.token_margins([1.0 + 3e-7, 1.0, -1.0, -2.0], [0, 1], [0.5, 0.5], inf, 1)
+    assert abs(m["order"] - 3e-7) < 1e-12 and T.is_tied(m, _TB), m
+    # (c) |c - tau| of a non-top-1 slot
+    m = T.token_margins([3.0, 2.0, 1.0, 0.0], [0, 1, 2], [0.6, 0.3000004, 0.1], 0.3, 1)
+    assert abs(m["tau"] - 4e-7) < 1e-12 and T.is_tied(m, _TB), m
+    # (d) the top-1 slot is never a candidate, so its distance to tau is no margin
+    m = T.token_margins([3.0, 2.0, 1.0, 0.0], [0, 1, 2], [0.3000004, 0.2, 0.1], 0.3, 1)
+    assert abs(m["tau"] - 0.1) < 1e-12 and not T.is_tied(m, _TB), m
+    # tau = +inf (the clip branch) has no tau margin
+    assert T.token_margins([3.0, 2.0, 1.0], [0, 1], [0.6, 0.4], inf, 1)["tau"] == inf
+    # (e) restore order: only with m_min > 1, over the non-top-1 contributions
+    c = [0.5, 0.2000003, 0.2, 0.05]
+    m1 = T.token_margins([4.0, 3.0, 2.0, 1.0, 0.0], [0, 1, 2, 3], c, 0.9, 1)
+    m2 = T.token_margins([4.0, 3.0, 2.0, 1.0, 0.0], [0, 1, 2, 3], c, 0.9, 2)
+    assert m1["restore"] == inf and not T.is_tied(m1, _TB), m1
+    assert abs(m2["restore"] - 3e-7) < 1e-12 and T.is_tied(m2, _TB), m2
+    # top-1's c is no restore candidate either
+    m = T.token_margins([4.0, 3.0, 2.0, 1.0, 0.0], [0, 1, 2, 3], [0.2000001, 0.2, 0.1, 0.05], 0.9, 2)
+    assert abs(m["restore"] - 0.05) < 1e-12 and not T.is_tied(m, _TB), m
+    # the band is strict: a margin of exactly the band is not a tie
+    assert not T.is_tied(dict(boundary=_TB, order=1.0, tau=1.0, restore=np.inf), _TB)
+    assert T.is_tied(dict(boundary=np.nextafter(_TB, 0.0), order=1.0, tau=1.0, restore=np.inf), _TB)
+
+
+def check_ties_admissible_hand_tokens():
+    T = oracle.ties
+    eps = 1e-6
+    ones = np.ones(6)
+    z = [2.0, 1.0, 0.5, -1.0, -2.0, -3.0]
+    idx = [0, 1, 2]
+    pi, g, c = _tok(z, idx)
+
+    def adm(keep, tau, gidx=idx, zz=z, p=pi, a=ones, m_min=1, band=_TB):
+        return T.admissible_token(zz, p, gidx, keep, a, a, tau, m_min, eps, band)[0]
+
+    # slot 2's c within the band of tau: either decision is admissible
+    tau = c[2] + 5e-7
+    assert adm([1, 1, 0], tau) and adm([1, 1, 1], tau)
+    assert not adm([1, 0, 1], tau), "slot 1 (c far above tau) skipped"
+    assert not adm([0, 1, 1], tau), "top-1 skipped"
+    # c clearly below tau: the slot must be skipped
+    tau = c[2] + 5e-6
+    assert adm([1, 1, 0], tau) and not adm([1, 1, 1], tau)
+    # c clearly above tau: the slot must be kept
+    tau = c[2] - 5e-6
+    assert adm([1, 1, 1], tau) and not adm([1, 1, 0], tau)
+    # exactly one band below tau is outside the (strict) band: a clear skip (a band of
+    # 2^-20, so that tau - c is exactly the band in fp64)
+    b2 = 2.0 ** -20
+    tau = c[2] + b2
+    assert tau - c[2] == b2
+    assert adm([1, 1, 0], tau, band=b2) and not adm([1, 1, 1], tau, band=b2)
+    # top-k set: expert 3 within the band of expert 2 may replace it, not when clearly smaller
+    for gap, ok in ((4e-7, True), (4e-6, False)):
+        zb = [2.0, 1.0, 0.5 + gap, 0.5, -2.0, -3.0]
+        pb, _, cb = _tok(zb, [0, 1, 3])
+        assert adm([1, 1, 1], 0.0, gidx=[0, 1, 3], zz=zb, p=pb) == ok, gap
+    # slot order: two near-equal logits may come in either order, not clearly inverted ones
+    for gap, ok in ((4e-7, True), (4e-6, False)):
+        zo = [2.0 + gap, 2.0, 0.5, -1.0, -2.0, -3.0]
+        po, _, _ = _tok(zo, [1, 0, 2])
+        assert adm([1, 1, 1], 0.0, gidx=[1, 0, 2], zz=zo, p=po) == ok, gap
+    # m_min = 2 restore: slots 1 and 2 have near-equal c (tables offset the gates), all three
+    # non-top-1 slots are below tau, so exactly one is restored, the one with the largest c
+    z4 = [3.0, 2.0, 1.5, 1.0, -1.0, -2.0]
+    i4 = [0, 1, 2, 3]
+    e4 = np.exp(np.asarray(z4) - 3.0)
+    g4 = e4[i4] / e4[i4].sum()
+    for delta, tie in ((1e-6, True), (1e-3, False)):
+        a4 = np.ones(6)
+        a4[2] = (g4[1] / g4[2]) * (1.0 - delta)            # s_2 = s_1 (1 - delta)
+        p4, _, c4 = _tok(z4, i4, a4)
+        assert c4[1] > c4[2] > c4[3] and (abs(c4[1] - c4[2]) < _TB) == tie, (c4, delta)
+        tau4 = c4[1] + 0.05
+        assert adm([1, 1, 0, 0], tau4, gidx=i4, zz=z4, p=p4, a=a4, m_min=2)
+        assert adm([1, 0, 1, 0], tau4, gidx=i4, zz=z4, p=p4, a=a4, m_min=2) == tie
+        assert not adm([1, 0, 0, 1], tau4, gidx=i4, zz=z4, p=p4, a=a4, m_min=2), "restored the lowest c"
+        assert not adm([1, 1, 1, 0], tau4, gidx=i4, zz=z4, p=p4, a=a4, m_min=2), "restored one too many"
+        assert not adm([1, 0, 0, 0], tau4, gidx=i4, zz=z4, p=p4, a=a4, m_min=2), "m_min not met"
+
+
+def check_ties_compare_decisions():
+    """Token 0 clear and equal; token 1 clear but different (a mismatch); token 2
+    tied (c within the band) and differing admissibly; token 3 tied and differing
+    inadmissibly (a clearly kept slot skipped)."""
+    T = oracle.ties
+    eps = 1e-6
+    ones = np.ones(6)
+    z0 = [2.0, 1.0, 0.5, -1.0, -2.0, -3.0]
+    idx = [0, 1, 2]
+    _, _, c0 = _tok(z0, idx)
+    tau = c0[2] + 5e-7                       # tokens 2 and 3: slot 2 within the band of tau
+    z1 = [2.0, 1.0, 0.0, -1.0, -2.0, -3.0]  # tokens 0 and 1: slot 2's c far below tau
+    _, _, c1 = _tok(z1, idx)
+    assert abs(c1[2] - tau) > 1e-3
+    zs = np.array([z1, z1, z0, z0])
+    pis = np.stack([_tok(zz, idx)[0] for zz in zs])
+    cs = np.stack([c1, c1, c0, c0])
+    okeep = np.array([[1, 1, 0], [1, 1, 0], [1, 1, 0], [1, 1, 0]], bool)
+    oidx = np.array([idx] * 4)
+    gkeep = np.array([[1, 1, 0], [1, 1, 1], [1, 1, 1], [1, 0, 0]], bool)
+    # token 1: c1[2] is clearly below tau, so the oracle skips it; keeping it is a mismatch
+    assert c1[2] < tau
+    rep = T.compare_decisions(zs, pis, oidx, okeep, cs, oidx.copy(), gkeep, ones, ones, tau, 1, eps)
+    assert rep["n_tokens"] == 4
+    assert rep["tied"] == [2, 3], rep
+    assert rep["mismatch_untied"] == [1], rep
+    assert rep["differing_tied"] == [2, 3], rep
+    assert rep["inadmissible"] == [3], rep
+    # identical decisions everywhere: tied tokens are still counted, nothing else reported
+    rep = T.compare_decisions(zs, pis, oidx, okeep, cs, oidx.copy(), okeep.copy(), ones, ones, tau, 1, eps)
+    assert rep["tied"] == [2, 3] and not rep["mismatch_untied"] and not rep["differing_tied"]
+    assert not rep["inadmissible"]
+
+
 ALL_CHECKS = [v for k, v in sorted(globals().items()) if k.startswith("check_")]

@@ -1,6 +1,8 @@
 """Plant plausible mistakes in the CPU oracle and confirm that the pins catch
 each one (a dropped term, a wrong sign, order or index, a swapped operand).
 Every mutant lives only inside this test, on the CPU."""
+from itertools import combinations
+
 import numpy as np
 import pytest
 
@@ -11,6 +13,7 @@ F = oracle.forward
 TB = oracle.tables
 TAU = oracle.tau
 PL = oracle.plan
+TIES = oracle.ties
 
 
 def _rms_abs(x, gamma, rms_eps):
@@ -161,6 +164,90 @@ def _plan_token_desc(topk_idx, keep, N):
                 slot_row=slot_row)
 
 
+def _margins_variant(kind):
+    def fn(z_row, idx_row, c_row, tau, m_min):
+        z_row = np.asarray(z_row, float)
+        k = len(idx_row)
+        zs = np.sort(z_row)[::-1]
+        if kind == "boundary_off_by_one":
+            boundary = zs[k] - zs[k + 1] if k + 1 < len(zs) else np.inf
+        else:
+            boundary = zs[k - 1] - zs[k] if k < len(zs) else np.inf
+        ids = np.sort(np.asarray(idx_row)) if kind == "order_unsorted" else np.asarray(idx_row)
+        ztop = z_row[ids]
+        order = np.min(ztop[:-1] - ztop[1:]) if k > 1 else np.inf
+        call = np.asarray(c_row, float)
+        c = call if kind == "tau_includes_top1" else call[1:]
+        tau_m = np.min(np.abs(c - tau)) if np.isfinite(tau) and c.size else np.inf
+        restore = np.inf
+        if (m_min > 1 or kind == "restore_any_m_min") and c.size > 1:
+            cs = np.sort(c)
+            restore = np.min(cs[1:] - cs[:-1])
+        return dict(boundary=boundary, order=order, tau=tau_m, restore=restore)
+    return fn
+
+
+def _is_tied_inclusive(m, band=TIES.BAND):
+    return min(m.values()) <= band
+
+
+def _admissible_variant(kind):
+    def fn(z_row, pi_row, gpu_idx_row, gpu_keep_row, a_gsp, a_rcr, tau, m_min, eps, band=TIES.BAND,
+           fusion="max"):
+        z_row = np.asarray(z_row, float)
+        idx = np.asarray(gpu_idx_row, dtype=np.int64)
+        keep = np.asarray(gpu_keep_row, dtype=bool)
+        k, N = idx.size, z_row.size
+        if len(set(idx.tolist())) != k or idx.min() < 0 or idx.max() >= N:
+            return False, "ids"
+        zt = z_row[idx]
+        if kind != "no_order_check" and k > 1 and np.any(zt[:-1] < zt[1:] - band):
+            return False, "order"
+        others = np.setdiff1d(np.arange(N), idx)
+        if kind != "no_topk_set_check" and others.size and zt.min() < z_row[others].max() - band:
+            return False, "set"
+        if not keep[0]:
+            return False, "top1"
+        top = np.asarray(pi_row, float)[idx]
+        g = top / top.sum()
+        c = F.contributions(g, np.asarray(a_gsp, float)[idx], np.asarray(a_rcr, float)[idx], eps, fusion)[0]
+        skip_final = {i for i in range(1, k) if not keep[i]}
+        if kind == "band_inclusive":
+            ambiguous = [i for i in range(1, k) if abs(c[i] - tau) <= band]
+        else:
+            ambiguous = [i for i in range(1, k) if abs(c[i] - tau) < band]
+        clear_skip = {i for i in range(1, k) if c[i] < tau and i not in ambiguous}
+        if kind == "ignore_clear_skip":
+            clear_skip = set()
+        for r in range(len(ambiguous) + 1):
+            for extra in combinations(ambiguous, r):
+                s0 = clear_skip | set(extra)
+                need = max(0, m_min - (k - len(s0)))
+                if kind != "skip_not_subset" and not skip_final <= s0:
+                    continue
+                restored = s0 - skip_final
+                if kind == "skip_not_subset":
+                    restored = set()
+                    need = 0
+                if len(restored) != need:
+                    continue
+                if kind == "restore_order_ignored" or all(c[a] >= c[b] - band for a in restored for b in skip_final):
+                    return True, "ok"
+        return False, "mask"
+    return fn
+
+
+def _compare_no_admissibility(z, pi, oracle_idx, oracle_keep, c, gpu_idx, gpu_keep, a_gsp, a_rcr, tau, m_min,
+                              eps, band=TIES.BAND, fusion="max"):
+    rep = _ORIG_COMPARE(z, pi, oracle_idx, oracle_keep, c, gpu_idx, gpu_keep, a_gsp, a_rcr, tau, m_min, eps,
+                        band, fusion)
+    rep["inadmissible"] = []
+    return rep
+
+
+_ORIG_COMPARE = TIES.compare_decisions
+
+
 MUTANTS = {
     "rmsnorm_mean_abs": [(F, "rmsnorm", _rms_abs)],
     "rmsnorm_no_gamma": [(F, "rmsnorm", _rms_no_gamma)],
@@ -186,6 +273,19 @@ MUTANTS = {
     "tau_floor": [(TAU, "tau_for_budget", _tau_floor)],
     "tau_off_by_one": [(TAU, "tau_for_budget", _tau_off_by_one)],
     "plan_token_descending": [(PL, "dispatch_plan", _plan_token_desc)],
+    "ties_boundary_off_by_one": [(TIES, "token_margins", _margins_variant("boundary_off_by_one"))],
+    "ties_order_unsorted": [(TIES, "token_margins", _margins_variant("order_unsorted"))],
+    "ties_tau_includes_top1": [(TIES, "token_margins", _margins_variant("tau_includes_top1"))],
+    "ties_restore_any_m_min": [(TIES, "token_margins", _margins_variant("restore_any_m_min"))],
+    "ties_band_inclusive": [(TIES, "is_tied", _is_tied_inclusive)],
+    "ties_admissible_band_inclusive": [(TIES, "admissible_token", _admissible_variant("band_inclusive"))],
+    "ties_admissible_ignores_clear_skip": [(TIES, "admissible_token", _admissible_variant("ignore_clear_skip"))],
+    "ties_admissible_skip_not_subset": [(TIES, "admissible_token", _admissible_variant("skip_not_subset"))],
+    "ties_admissible_restore_order_ignored": [(TIES, "admissible_token",
+                                               _admissible_variant("restore_order_ignored"))],
+    "ties_admissible_no_topk_set_check": [(TIES, "admissible_token", _admissible_variant("no_topk_set_check"))],
+    "ties_admissible_no_order_check": [(TIES, "admissible_token", _admissible_variant("no_order_check"))],
+    "ties_compare_no_admissibility": [(TIES, "compare_decisions", _compare_no_admissibility)],
 }
 
 
