@@ -32,14 +32,15 @@
 extern "C" {
 #endif
 
-#define ACE_ABI_VERSION 2
+#define ACE_ABI_VERSION 3
 
 typedef enum {
   ACE_OK = 0,
   ACE_ERR_INVALID_ARG = -1, /* NULL required pointer, bad shape, misaligned pointer, bad scalar */
   ACE_ERR_UNSUPPORTED = -2, /* valid but outside the compiled shape/dtype set (see ace_moe_forward) */
   ACE_ERR_WORKSPACE = -3,   /* workspace NULL or smaller than ace_moe_workspace_size() */
-  ACE_ERR_HIP = -4          /* a HIP launch reported an error */
+  ACE_ERR_HIP = -4,         /* a HIP launch reported an error */
+  ACE_ERR_SCRATCH_LIMIT = -5 /* ace_moe_forward_noalloc: the layer needs more than its static scratch */
 } ace_status;
 
 typedef enum { ACE_F32 = 0, ACE_BF16 = 1 } ace_dtype;
@@ -138,6 +139,33 @@ size_t ace_moe_workspace_size(const ace_moe_desc *desc);
 ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
                            const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
                            void *stream);
+
+/*
+ * ace_moe_forward without a workspace argument and without any allocation, for
+ * callers that cannot allocate device memory: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Same arguments, semantics,
+ * kernels and results as ace_moe_forward (bit-identical outputs), except that the
+ * scratch memory is a static array of ACE_NOALLOC_SCRATCH_BYTES inside the
+ * library's code object, one per GPU, which that GPU holds from the first call on
+ * it until the process ends.  The call runs on the current device (the one
+ * `stream` belongs to) and allocates nothing: no hipMalloc, no hipFree, no
+ * allocating library routine.  The first call on a device looks up that device's
+ * array address once (hipGetSymbolAddress; no allocation).
+ *   Limit: layers whose ace_moe_workspace_size(desc) exceeds
+ *   ACE_NOALLOC_SCRATCH_BYTES -> ACE_ERR_SCRATCH_LIMIT before any launch (for the
+ *   d = 2048, N = 128, k = 8, m = 768 bf16 layer that is T above 1361 tokens;
+ *   decode batches fit easily).
+ *   Concurrency: every call on one GPU uses that GPU's one array, which keeps the
+ *   last call's contents (no call depends on them).  Calls that can overlap on one
+ *   GPU (different streams without ordering, or host threads racing on streams of
+ *   the same device) race on the array and give wrong results; order them on one
+ *   stream, or use ace_moe_forward with separate workspaces.
+ * Errors: as ace_moe_forward, ACE_ERR_SCRATCH_LIMIT as above, ACE_ERR_HIP if the
+ * device or its array cannot be found.
+ */
+#define ACE_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+ace_status ace_moe_forward_noalloc(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
+                                   const ace_moe_outputs *out, void *stream);
 
 /*
  * Stage timing, for measurement only (computing the layer never needs it).

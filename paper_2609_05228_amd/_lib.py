@@ -18,6 +18,8 @@ ACE_ERR_INVALID_ARG = -1
 ACE_ERR_UNSUPPORTED = -2
 ACE_ERR_WORKSPACE = -3
 ACE_ERR_HIP = -4
+ACE_ERR_SCRATCH_LIMIT = -5
+NOALLOC_SCRATCH_BYTES = 64 << 20  # ACE_NOALLOC_SCRATCH_BYTES
 ACE_F32 = 0
 ACE_BF16 = 1
 ACE_SKIP_DISABLE = 1 << 0
@@ -70,6 +72,9 @@ def lib() -> ctypes.CDLL:
                                       ctypes.POINTER(Outputs), ctypes.c_void_p, ctypes.c_size_t,
                                       ctypes.c_void_p]
         L.ace_moe_forward.restype = ctypes.c_int
+        L.ace_moe_forward_noalloc.argtypes = [ctypes.POINTER(Desc), ctypes.c_void_p, ctypes.POINTER(Weights),
+                                              ctypes.POINTER(Outputs), ctypes.c_void_p]
+        L.ace_moe_forward_noalloc.restype = ctypes.c_int
         L.ace_status_string.argtypes = [ctypes.c_int]
         L.ace_status_string.restype = ctypes.c_char_p
         L.ace_abi_version.argtypes = []
@@ -133,6 +138,13 @@ def forward_raw(desc: Desc, x_ptr: int, weights: Weights, outputs: Outputs, ws_p
     return int(lib().ace_moe_forward(ctypes.byref(desc), ctypes.c_void_p(x_ptr), ctypes.byref(weights),
                                      ctypes.byref(outputs), ctypes.c_void_p(ws_ptr),
                                      ctypes.c_size_t(ws_bytes), ctypes.c_void_p(stream)))
+
+
+def forward_noalloc_raw(desc: Desc, x_ptr: int, weights: Weights, outputs: Outputs, stream: int) -> int:
+    """ace_moe_forward_noalloc (static per-device scratch, no workspace argument, no
+    allocation) on plain integers/structs; returns the ace_status."""
+    return int(lib().ace_moe_forward_noalloc(ctypes.byref(desc), ctypes.c_void_p(x_ptr), ctypes.byref(weights),
+                                             ctypes.byref(outputs), ctypes.c_void_p(stream)))
 
 
 TAU_MAX_Q = 8

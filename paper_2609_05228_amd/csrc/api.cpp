@@ -4,7 +4,9 @@
 //   -> plan (expert scan, then prefix sum, permutation and M tiles)
 //   -> grouped gate/up + SwiGLU -> grouped down
 //   -> [shared expert: dense gate/up -> dense down] -> gate-weighted combine.
-// Everything is enqueued on the caller's stream; nothing is allocated.
+// Everything is enqueued on the caller's stream; nothing is allocated (the
+// no-allocation variant runs in a static per-device scratch array instead of a
+// caller workspace).
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -165,6 +167,44 @@ void mark(hipEvent_t *slot, int i, hipStream_t s) {
   if (slot) (void)hipEventRecord(slot[i], s);
 }
 
+// ---------------------------------------------------------------- static scratch
+// Workspace of ace_moe_forward_noalloc: one array per GPU, part of this library's
+// code object (each GPU holds its own copy from the first use until the process
+// ends).  In host code `scratch` names a host-side stand-in, not device memory: its
+// device address is looked up once per device with hipGetSymbolAddress and only
+// that address is ever handed to kernels.
+static __device__ __align__(256) uint8_t scratch[ACE_NOALLOC_SCRATCH_BYTES];
+
+struct ScratchTable {
+  std::mutex mu;
+  std::vector<void *> ptr;  // device id -> address of that device's scratch (null: not yet looked up)
+};
+ScratchTable g_scratch;
+
+// address of the current device's scratch, looked up (with that device current) on
+// the first call on the device
+hipError_t scratch_on_current_device(void **out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch.mu);
+  if (static_cast<size_t>(dev) >= g_scratch.ptr.size()) g_scratch.ptr.resize(static_cast<size_t>(dev) + 1, nullptr);
+  if (!g_scratch.ptr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || (reinterpret_cast<uintptr_t>(p) & (kAlign - 1))) return hipErrorInvalidSymbol;
+    g_scratch.ptr[dev] = p;
+  }
+  *out = g_scratch.ptr[dev];
+  return hipSuccess;
+}
+
+ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
+                        const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
+                        void *stream_ptr);
+
 }  // namespace
 
 extern "C" {
@@ -295,6 +335,9 @@ const char *ace_status_string(int s) {
     case ACE_ERR_UNSUPPORTED: return "ACE_ERR_UNSUPPORTED: shape or dtype outside the compiled set";
     case ACE_ERR_WORKSPACE: return "ACE_ERR_WORKSPACE: workspace missing or too small";
     case ACE_ERR_HIP: return "ACE_ERR_HIP: a HIP launch failed";
+    case ACE_ERR_SCRATCH_LIMIT:
+      return "ACE_ERR_SCRATCH_LIMIT: the layer needs more than the ACE_NOALLOC_SCRATCH_BYTES of static scratch "
+             "(use ace_moe_forward with a workspace)";
     default: return "unknown ace_status";
   }
 }
@@ -302,6 +345,28 @@ const char *ace_status_string(int s) {
 ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
                            const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
                            void *stream_ptr) {
+  return forward_impl(desc, x, w, out, workspace, workspace_bytes, stream_ptr);
+}
+
+ace_status ace_moe_forward_noalloc(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
+                                   const ace_moe_outputs *out, void *stream_ptr) {
+  const ace_status v = validate(desc, x, w, out);
+  if (v != ACE_OK) return v;
+  if (desc->T == 0) return ACE_OK;
+  const size_t need = layout_for(*desc).total;
+  if (need > ACE_NOALLOC_SCRATCH_BYTES) return ACE_ERR_SCRATCH_LIMIT;
+  void *ws = nullptr;
+  if (scratch_on_current_device(&ws) != hipSuccess) return ACE_ERR_HIP;
+  return forward_impl(desc, x, w, out, ws, ACE_NOALLOC_SCRATCH_BYTES, stream_ptr);
+}
+
+}  // extern "C"
+
+namespace {
+
+ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
+                        const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
+                        void *stream_ptr) {
   const ace_status v = validate(desc, x, w, out);
   if (v != ACE_OK) return v;
   const ace_moe_desc &d = *desc;
@@ -512,4 +577,4 @@ ace_status ace_moe_forward(const ace_moe_desc *desc, const void *x, const ace_mo
   return ACE_OK;
 }
 
-}  // extern "C"
+}  // namespace

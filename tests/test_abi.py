@@ -32,7 +32,8 @@ def test_library_exports_every_declared_function():
 def test_version_and_status_strings():
     m = re.search(r"#define ACE_ABI_VERSION (\d+)", open(HEADER).read())
     assert ace.abi_version() == int(m.group(1))
-    for code, word in [(0, "ACE_OK"), (-1, "INVALID_ARG"), (-2, "UNSUPPORTED"), (-3, "WORKSPACE"), (-4, "HIP")]:
+    for code, word in [(0, "ACE_OK"), (-1, "INVALID_ARG"), (-2, "UNSUPPORTED"), (-3, "WORKSPACE"), (-4, "HIP"),
+                       (-5, "SCRATCH_LIMIT")]:
         assert word in ace.status_string(code)
     assert "unknown" in ace.status_string(12345)
 
@@ -162,3 +163,25 @@ def test_build_tables_validation():
     assert call(w=_lib.Weights(FAKE + 8, FAKE, 0, FAKE, FAKE, FAKE, 0, 0, 0, 0, 0)) == _lib.ACE_ERR_INVALID_ARG
     assert call(ws=0) == _lib.ACE_ERR_WORKSPACE
     assert call(ws_bytes=need - 1) == _lib.ACE_ERR_WORKSPACE
+
+def test_noalloc_validates_and_refuses_oversized_layers_on_the_host():
+    """The no-allocation entry point checks its arguments like ace_moe_forward and
+    refuses a layer whose workspace exceeds its static scratch before touching any
+    device (these calls return without a GPU)."""
+    w = _lib.Weights(*([FAKE] * 3 + [FAKE] * 3 + [0, 0, 0] + [FAKE, FAKE]))
+    w.b_router = 0
+    o = _lib.Outputs(FAKE, FAKE, FAKE, 0, 0, 0, 0, 0)
+    big = _desc(T=4096, d=2048, N=128, k=8, m=768)
+    m = re.search(r"#define ACE_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", open(HEADER).read())
+    assert m and int(m.group(1)) << int(m.group(2)) == _lib.NOALLOC_SCRATCH_BYTES
+    assert ace.workspace_size(big) > _lib.NOALLOC_SCRATCH_BYTES
+    assert _lib.forward_noalloc_raw(big, FAKE, w, o, 0) == _lib.ACE_ERR_SCRATCH_LIMIT
+    edge = _desc(T=1362, d=2048, N=128, k=8, m=768)
+    assert ace.workspace_size(edge) > _lib.NOALLOC_SCRATCH_BYTES
+    assert _lib.forward_noalloc_raw(edge, FAKE, w, o, 0) == _lib.ACE_ERR_SCRATCH_LIMIT
+    assert ace.workspace_size(_desc(T=1361, d=2048, N=128, k=8, m=768)) <= _lib.NOALLOC_SCRATCH_BYTES
+    assert _lib.forward_noalloc_raw(_desc(k=9, N=8), FAKE, w, o, 0) == _lib.ACE_ERR_INVALID_ARG
+    assert _lib.forward_noalloc_raw(_desc(d=200), FAKE, w, o, 0) == _lib.ACE_ERR_UNSUPPORTED
+    assert _lib.forward_noalloc_raw(_desc(T=0), FAKE, w, o, 0) == _lib.ACE_OK
+    o0 = _lib.Outputs(0, FAKE, FAKE, 0, 0, 0, 0, 0)
+    assert _lib.forward_noalloc_raw(_desc(), FAKE, w, o0, 0) == _lib.ACE_ERR_INVALID_ARG
