@@ -166,7 +166,7 @@ __device__ __forceinline__ int pending_ok(int kt, int nk, int na) {
 // banks.  Wave w computes row blocks wr, wr+RW, ... (wr = w/2) against the CG/2
 // column groups starting at wc*CG/2 (wc = w%2).
 template <bool GATEUP, int MB, int CG, int KH, int W>
-__device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, int mrot, uint8_t *smem) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, int erot, uint8_t *smem) {
   static_assert(KH == 2, "8-row DMA units span a 64-wide K stage");
   using P = Pipe<MB, CG, KH, W>;
   constexpr int RW = W / 2;    // waves along the rows
@@ -232,12 +232,15 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     for (int c = 0; c < 2 * CW; ++c) acc[i][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   const int nk = K / BK;
-  // Pipeline stage s covers K block (s + k0) % nk, k0 set by the M tile.  M tiles
-  // start at different K blocks: rows 4 KB apart (d = 2048 bf16) read at one K
-  // offset by every workgroup at once concentrate on a few HBM channels and
-  // stream ~20% slower.  The N tiles of one M tile keep one K order, so the
-  // activation rows they all read are shared in their XCD's L2.
-  const int k0 = mrot % nk;
+  // Pipeline stage s covers K block (s + k0) % nk, k0 set by the tile's expert.
+  // Experts start at different K blocks: rows 4 KB apart (d = 2048 bf16) read at
+  // one K offset by every workgroup at once concentrate on a few HBM channels and
+  // stream ~20% slower.  Every tile of one expert keeps one K order: the N tiles
+  // of an M tile share its activation rows in their XCD's L2, and the M tiles of a
+  // large expert that run at the same time on one XCD share its weight rows
+  // (starting each M tile at its own block left them out of step, and the
+  // wider-pool gate/up fetched three times its weight bytes from beyond L2).
+  const int k0 = erot % nk;
   auto kofs = [&](int s) { return (s + k0 < nk ? s + k0 : s + k0 - nk) * BK; };
   // weight units of stage s into LDS stage base st: weights that no other M tile
   // reads stream with the non-temporal hint; weights shared by several M tiles
@@ -345,14 +348,16 @@ __global__ __launch_bounds__(W * 64) void grouped_gemm_bf16_kernel(GemmArgs a) {
   if (!ti.valid) return;
   __shared__ __align__(16) uint8_t smem[kLdsBytes];
   const int blocks = (ti.rows + 15) >> 4;
+  // K rotation key: the expert (the appended dense expert gets its own)
+  const int erot = ti.sh ? 0x155 : ti.e;
   if (blocks <= 4)
-    gemm_tile<GATEUP, 4, CG, stage_halves<CG>(), W>(a, ti, nt, grp, smem);
+    gemm_tile<GATEUP, 4, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
   else if (blocks <= 8)
-    gemm_tile<GATEUP, 8, CG, stage_halves<CG>(), W>(a, ti, nt, grp, smem);
+    gemm_tile<GATEUP, 8, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
   else if (blocks <= 12)
-    gemm_tile<GATEUP, 12, CG, stage_halves<CG>(), W>(a, ti, nt, grp, smem);
+    gemm_tile<GATEUP, 12, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
   else
-    gemm_tile<GATEUP, 16, CG, stage_halves<CG>(), W>(a, ti, nt, grp, smem);
+    gemm_tile<GATEUP, 16, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
 }
 
 // ------------------------------------------------------------------ fp32 (tiled FMA)
