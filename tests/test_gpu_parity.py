@@ -11,7 +11,7 @@ import torch
 
 import oracle
 import synth
-from gpu_helpers import DEV, device_layer, full_check, run_gpu
+from gpu_helpers import DEV, device_layer, full_check, run_gpu, with_f64_weights
 
 sys.path.insert(0, os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden"))
 import make_tables  # noqa: E402
@@ -26,7 +26,7 @@ def _taus(L, a_gsp, a_rcr, qs, m_min=1, fusion="max"):
 
 
 def _report(name, r):
-    print(f"[{name}] rel_l2={r['rel_l2']:.3e} worst_token={r['worst_token']:.3e} "
+    print(f"[{name}] rel_l2={r['rel_l2']:.3e} worst_token={r['worst_token']:.3e} checked={r['n_checked']} "
           f"tied={len(r['ties']['tied'])} differing_tied={len(r['ties']['differing_tied'])} "
           f"skip={1 - r['gpu']['keep'].mean():.4f}", flush=True)
 
@@ -144,7 +144,8 @@ def prefill():
     gold = make_tables.load("prefill_4096")
     assert gold["config"]["T"] == cfg.T and gold["config"]["N"] == cfg.N and gold["config"]["seed"] == cfg.seed
     L = synth.make_layer(cfg)
-    return L, device_layer(L), np.array(gold["a_gsp"], np.float32), np.array(gold["a_rcr"], np.float32), gold
+    D = device_layer(L)
+    return with_f64_weights(L), D, np.array(gold["a_gsp"], np.float32), np.array(gold["a_rcr"], np.float32), gold
 
 
 SAMPLE = list(range(0, 4096, 64)) + [4095]
@@ -152,12 +153,20 @@ SAMPLE = list(range(0, 4096, 64)) + [4095]
 
 @pytest.mark.parametrize("q", ["0.5", "0.25"])
 def test_prefill_4096(prefill, q):
+    """Every decision; outputs on a token sample plus every token routed to the two
+    experts with the most kept rows (at q = 0.25 the largest experts fill a whole
+    256-row M tile, at q = 0.5 they take the 192-row tile body), so every row block
+    and every feature/column tile of those experts' GEMM tiles is checked."""
     L, D, ag, ar, gold = prefill
     tau = gold["tau_f32"][q]
-    r = full_check(L, D, ag, ar, tau, tokens=SAMPLE)
+    r = full_check(L, D, ag, ar, tau, tokens=SAMPLE, hot=(2, None))
     _report(f"prefill_4096 q={q} tau={tau}", r)
     realised = 1 - r["gpu"]["keep"].mean()
     assert abs(realised - float(q)) < 1e-3
+    counts = r["gpu"]["counts"]
+    assert r["n_checked"] >= len(SAMPLE) + counts.max() - 2
+    if q == "0.25":
+        assert counts.max() >= 256, "the largest expert fills a 256-row tile"
 
 
 def test_prefill_4096_skip_disable(prefill):
@@ -168,13 +177,15 @@ def test_prefill_4096_skip_disable(prefill):
 
 @pytest.mark.parametrize("B", [1, 8, 32, 64])
 def test_decode(prefill, B):
+    """Four seeded decode steps per batch size, every token's decisions and output."""
     L, D, ag, ar, gold = prefill
     cfg = L["cfg"].with_(T=B)
-    xs = synth.decode_inputs(cfg, B, step=0)
-    Ld = dict(L, x=xs, cfg=cfg)
-    Dd = dict(D, x=torch.from_numpy(xs).to(DEV).to(torch.bfloat16))
-    r = full_check(Ld, Dd, ag, ar, gold["tau_f32"]["0.5"])
-    _report(f"decode B={B}", r)
+    for step in range(4):
+        xs = synth.decode_inputs(cfg, B, step=step)
+        Ld = dict(L, x=xs, cfg=cfg)
+        Dd = dict(D, x=torch.from_numpy(xs).to(DEV).to(torch.bfloat16))
+        r = full_check(Ld, Dd, ag, ar, gold["tau_f32"]["0.5"])
+        _report(f"decode B={B} step={step}", r)
 
 
 # ------------------------------------------------------------------ full-size wider pool (256 experts, shared expert, Zipf router)
@@ -184,16 +195,19 @@ def zipf():
     gold = make_tables.load("zipf_256")
     assert gold["config"]["T"] == cfg.T and gold["config"]["N"] == cfg.N and gold["config"]["seed"] == cfg.seed
     L = synth.make_layer(cfg)
-    return L, device_layer(L), np.array(gold["a_gsp"], np.float32), np.array(gold["a_rcr"], np.float32), gold
+    D = device_layer(L)
+    return with_f64_weights(L), D, np.array(gold["a_gsp"], np.float32), np.array(gold["a_rcr"], np.float32), gold
 
 
 ZSAMPLE = list(range(0, 8192, 128)) + [8191]
 
 
 def test_zipf_256(zipf):
+    """Every decision; outputs on a token sample plus the tokens of the first full
+    256-row M tile and of the last rows of the most popular expert (7739 rows)."""
     L, D, ag, ar, gold = zipf
     tau = gold["tau_f32"]["0.5"]
-    r = full_check(L, D, ag, ar, tau, tokens=ZSAMPLE)
+    r = full_check(L, D, ag, ar, tau, tokens=ZSAMPLE, hot=(1, 256))
     _report(f"zipf_256 q=0.5 tau={tau}", r)
     assert abs((1 - r["gpu"]["keep"].mean()) - 0.5) < 1e-3
     counts = r["gpu"]["counts"]
