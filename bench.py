@@ -9,14 +9,15 @@ oracle-built values stored in tests/golden/ (inputs of the layer, like weights).
 
 One step = one full layer forward (RMSNorm, router, top-k, ACE skip mask,
 dispatch plan, grouped gate/up + SwiGLU, grouped down, combine) on inputs
-already resident in HBM.  Each step is timed with HIP events recorded on the
-layer's stream; `ms_per_step` is the median over exactly --steps steps after
+already resident in HBM.  Each step is timed with HIP events the library records
+on the layer's stream (timing-only, no system fence) from before RMSNorm to after
+the combine; `ms_per_step` is the median over exactly --steps steps after
 --warmup untimed ones (the mean is reported beside it).  Prints ONE JSON line
 with, besides the headline:
   * the same layer at skip ratios 0 (tau = 0), 0.25 and 0.5, and the plain top-k
     layer through the same kernels (the speedup baseline);
-  * per-stage times from HIP events the library records on the layer's stream
-    during the timed steps, and the roofline of the dominant kernel with the
+  * per-stage times from the same events, recorded by the library on the layer's
+    stream during the timed steps, and the roofline of the dominant kernel with the
     algorithmic bytes of the method (activated experts' weights);
   * decode batches 1/8/32/64 over seeded steps (tau transferred from prefill);
   * the wider-pool layer (256 experts, shared expert, Zipf router, 8192 tokens);
@@ -98,31 +99,27 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def event_times(fns, steps: int, warmup: int, torch, ace=None):
-    """Per-step ms of `steps` calls, each bracketed by HIP events on the current
-    stream (the layer's stream), after `warmup` untimed calls.  fns is one
-    callable or a list cycled through (one per seeded input).  With `ace`, the
-    library's per-stage events are recorded during the same timed calls and the
-    average ms per stage is returned as well."""
+def event_times(fns, steps: int, warmup: int, torch, ace):
+    """Per-step ms of `steps` layer calls after `warmup` untimed ones, and the average
+    ms per stage.  fns is one callable or a list cycled through (one per seeded input).
+    The library records HIP events on the layer's stream before its first stage and
+    after each stage of every timed call (timing-only events, created without a
+    system-scope fence, so they do not flush the caches between stages); a step's time
+    is the span from its first to its last event, i.e. the layer from RMSNorm to the
+    combine, and the stage times come from the same timed calls."""
     fns = fns if isinstance(fns, (list, tuple)) else [fns]
     for i in range(warmup):
         fns[i % len(fns)]()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     torch.cuda.synchronize()
-    if ace is not None:
-        ace.profile_begin(steps)
+    ace.profile_begin(steps)
     try:
         for i in range(steps):
-            ev[i][0].record()
             fns[i % len(fns)]()
-            ev[i][1].record()
     finally:
-        stages = None
-        if ace is not None:
-            tot, n = ace.profile_end()
-            stages = {k: v / max(n, 1) for k, v in tot.items()}
+        tot, n, calls = ace.profile_end(steps)
     torch.cuda.synchronize()
-    return [a.elapsed_time(b) for a, b in ev], stages
+    assert n == steps, (n, steps)
+    return [sum(c.values()) for c in calls], {k: v / max(n, 1) for k, v in tot.items()}
 
 
 def summary(ms_list) -> dict:
@@ -326,8 +323,7 @@ def main():
 
     def prefill_leg(tau_, skip_disable=False, steps=None, warmup=None, stages=True):
         fn, o, _ = make_step(D["x"], D, tabs, k, tau_, skip_disable)
-        ms_list, st = event_times(fn, steps or args.steps, args.warmup if warmup is None else warmup, torch,
-                                  ace if stages else None)
+        ms_list, st = event_times(fn, steps or args.steps, args.warmup if warmup is None else warmup, torch, ace)
         s = summary(ms_list)
         keep = o["keep"].cpu().numpy()
         counts = o["counts"].cpu().numpy()
@@ -356,7 +352,7 @@ def main():
                 f, o, ws = make_step(xs[s], D, tabs, k, tau, ws=ws)
                 fa.append(f)
                 outs.append(o)
-            eager_a, _ = event_times(fa, S, min(args.warmup, S), torch)
+            eager_a, _ = event_times(fa, S, min(args.warmup, S), torch, ace)
             ms_a = graph_steps(fa, 20)
             kb = np.stack([o["keep"].cpu().numpy() for o in outs])
             ib = np.stack([o["topk_idx"].cpu().numpy() for o in outs])
@@ -369,8 +365,9 @@ def main():
                            f"HIP events; per-step time = replay time / {S}; median over the replays",
                  "tokens_per_s": round(B / (sa["median"] * 1e-3), 1),
                  "eager_ms_per_step": round(se["median"], 5),
-                 "eager_note": "median of per-step HIP-event times of eager calls (includes the GPU's idle "
-                               "time while the host enqueues each step's kernels)",
+                 "eager_note": "median over the eager calls of each call's span of the library's timing "
+                               "events (includes the GPU's idle time while the host enqueues the "
+                               "call's kernels)",
                  "realised_skip": round(float(1 - kb.mean()), 5),
                  "experts_active_mean": round(float(ea.mean()), 2),
                  "alg_bytes_mean": int(byts.mean()),
@@ -382,7 +379,7 @@ def main():
                     f, o, ws = make_step(xs[s], D, tabs, k, tau, skip_disable=True, ws=ws)
                     ft.append(f)
                     outs_t.append(o)
-                eager_t, _ = event_times(ft, S, min(args.warmup, S), torch)
+                eager_t, _ = event_times(ft, S, min(args.warmup, S), torch, ace)
                 st_, set_ = summary(graph_steps(ft, 20)), summary(eager_t)
                 ea_t = np.array([int((o["counts"].cpu().numpy() > 0).sum()) for o in outs_t])
                 r.update({"topk_ms_per_step": round(st_["median"], 5),
@@ -414,7 +411,7 @@ def main():
         s_top, o_top, _ = make_step(ZW["x"], ZW, zt, zcfg.k, ztau, skip_disable=True, ws=ws)
         ms_a, st = event_times(s_ace, args.steps, args.warmup, torch, ace)
         # --ace-only (profiler runs): the plain layer once, untimed, for its expert count only
-        ms_t = [float("nan")] if args.ace_only else event_times(s_top, args.steps, args.warmup, torch)[0]
+        ms_t = [float("nan")] if args.ace_only else event_times(s_top, args.steps, args.warmup, torch, ace)[0]
         if args.ace_only:
             s_top()
         sa, stt = summary(ms_a), summary(ms_t)
@@ -502,28 +499,33 @@ def main():
                                                out=o, ws=ws))
             return fns, x_buf, y_buf
 
-        def run_chain(chain, x_in, ev=None):
-            """One pass; with ev = (layer events, add events) every layer call and every
-            residual add is bracketed by its own event pair."""
+        def run_chain(chain, x_in):
             fns, xb, yb = chain
             xb.copy_(x_in)
-            for li, f in enumerate(fns):
-                if ev is not None:
-                    ev[0][li][0].record()
+            for f in fns:
                 f()
-                if ev is not None:
-                    ev[0][li][1].record()
-                    ev[1][li][0].record()
                 xb.add_(yb)
-                if ev is not None:
-                    ev[1][li][1].record()
 
-        def new_events():
-            E = lambda: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))  # noqa: E731
-            return [E() for _ in range(n_layers)], [E() for _ in range(n_layers)]
-
-        def read_events(ev):
-            return (sum(a.elapsed_time(b) for a, b in ev[0]), sum(a.elapsed_time(b) for a, b in ev[1]))
+        def timed_passes(chain, inputs):
+            """Each pass over the chain (one per input) with the library's timing events
+            on every layer call: MoE ms of a pass = the sum of its layer calls' spans;
+            the whole pass (copy-in, layers, residual adds) is bracketed by two events."""
+            run_chain(chain, inputs[0])  # warm-up
+            torch.cuda.synchronize()
+            ends = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in inputs]
+            ace.profile_begin(n_layers * len(inputs))
+            try:
+                for (a, b), xi in zip(ends, inputs):
+                    a.record()
+                    run_chain(chain, xi)
+                    b.record()
+            finally:
+                _, n, calls = ace.profile_end(n_layers * len(inputs))
+            torch.cuda.synchronize()
+            spans = [sum(c.values()) for c in calls]
+            moe = [sum(spans[i * n_layers:(i + 1) * n_layers]) for i in range(len(inputs))]
+            whole = [a.elapsed_time(b) for a, b in ends]
+            return statistics.median(moe), statistics.median(whole)
 
         xp = torch.empty_like(x0)
         # score pass through the unskipped chain, then one global tau (App. C.1 on the device)
@@ -541,24 +543,11 @@ def main():
         log(f"stack: global tau {stau} from {n_layers * Ts * kk} slots, mapping {tau_ms:.3f} ms")
 
         keeps = torch.empty((n_layers, Ts, kk), dtype=torch.uint8, device=dev)
-
-        def timed_prefill(chain, reps=3):
-            run_chain(chain, x0)  # warm-up
-            moe, add = [], []
-            for _ in range(reps):
-                ev = new_events()
-                run_chain(chain, x0, ev)
-                torch.cuda.synchronize()
-                a, b = read_events(ev)
-                moe.append(a)
-                add.append(b)
-            return statistics.median(moe), statistics.median(add)
-
         ace_chain = make_chain(xp, stau, False, keep_out=keeps)
-        ms_ace, add_ace = timed_prefill(ace_chain)
+        ms_ace, whole_ace = timed_passes(ace_chain, [x0] * 3)
         per_layer = 1.0 - keeps.float().mean(dim=(1, 2)).cpu().numpy()
         top_chain = make_chain(xp, stau, True)
-        ms_top, _ = timed_prefill(top_chain)
+        ms_top, _ = timed_passes(top_chain, [x0] * 3)
         log(f"stack prefill: ACE {ms_ace:.2f} ms (MoE), plain top-k {ms_top:.2f} ms")
         del ace_chain, top_chain
 
@@ -571,22 +560,13 @@ def main():
         dec_ace = make_chain(xd, stau, False, keep_out=dkeep)
         dec_top = make_chain(xd, stau, True)
 
-        def decode_ms(chain, skip_acc=None):
-            run_chain(chain, xs[0])  # warm-up
-            evs = []
-            for s in range(S):
-                ev = new_events()
-                run_chain(chain, xs[s], ev)
-                evs.append(ev)
-                if skip_acc is not None:
-                    skip_acc += 1.0 - dkeep.float().mean(dim=(1, 2))
-            torch.cuda.synchronize()
-            moe = [read_events(ev) for ev in evs]
-            return statistics.median([a for a, _ in moe]), statistics.median([b for _, b in moe])
-
+        ms_dec, whole_dec = timed_passes(dec_ace, [xs[s] for s in range(S)])
+        ms_dec_top, _ = timed_passes(dec_top, [xs[s] for s in range(S)])
+        # per-layer realised skip ratio over the decode steps (an untimed pass)
         acc = torch.zeros(n_layers, device=dev)
-        ms_dec, add_dec = decode_ms(dec_ace, acc)
-        ms_dec_top, _ = decode_ms(dec_top)
+        for s in range(S):
+            run_chain(dec_ace, xs[s])
+            acc += 1.0 - dkeep.float().mean(dim=(1, 2))
         dec_skip = (acc / S).cpu().numpy()
         res = {"workload": f"stack_48: {n_layers} MoE layers of the 4096-token layer's shape (T=8192 prefill; "
                            f"decode B=32 x {S} seeded steps), seed per layer, residual chain x <- x + y, "
@@ -595,7 +575,7 @@ def main():
                "tables_ms_all_layers": round(tables_ms, 2), "tables_identical_to_oracle_layers": same,
                "prefill": {"moe_ms": round(ms_ace, 3), "tokens_per_s": round(Ts / (ms_ace * 1e-3), 1),
                            "topk_moe_ms": round(ms_top, 3), "speedup_vs_topk": round(ms_top / ms_ace, 4),
-                           "residual_add_ms": round(add_ace, 3),
+                           "chain_total_ms": round(whole_ace, 3),
                            "realised_skip_overall": round(float(per_layer.mean()), 5),
                            "realised_skip_per_layer": {"min": round(float(per_layer.min()), 5),
                                                        "max": round(float(per_layer.max()), 5),
@@ -603,14 +583,15 @@ def main():
                "decode_b32": {"moe_ms_per_step": round(ms_dec, 4), "tokens_per_s": round(B / (ms_dec * 1e-3), 1),
                               "topk_moe_ms_per_step": round(ms_dec_top, 4),
                               "speedup_vs_topk": round(ms_dec_top / ms_dec, 4),
-                              "residual_add_ms_per_step": round(add_dec, 4),
+                              "chain_total_ms_per_step": round(whole_dec, 4),
                               "realised_skip_overall": round(float(dec_skip.mean()), 5),
                               "realised_skip_per_layer": {"min": round(float(dec_skip.min()), 5),
                                                           "max": round(float(dec_skip.max()), 5),
                                                           "std": round(float(dec_skip.std()), 5)}},
-               "note": "MoE times are sums of per-layer HIP-event times (medians over 3 prefill passes and over "
-                       "the decode steps); the residual adds x <- x + y (torch, in place) are timed apart; "
-                       "decode skip ratios are averaged over the steps"}
+               "note": "MoE times are sums of the layer calls' spans of the library's timing events (medians "
+                       "over 3 prefill passes and over the decode steps); chain totals add the copy-in and "
+                       "the residual adds x <- x + y (torch, in place) and the launch gaps; decode skip "
+                       "ratios are averaged over the steps"}
         log(f"stack_48: {res}")
         del Ws, scores, keeps, dec_ace, dec_top, xs
         torch.cuda.empty_cache()
@@ -678,7 +659,9 @@ def main():
                                "ACE skip target 0.5 (seeded synthetic inputs)",
                    "T": T, "d": d, "N": N, "k": k, "m": m, "skip_target": float(args.q), "tau": tau,
                    "realised_skip": head["realised_skip"], "experts_active": e_act, "kept_slots": n_kept},
-        "timing": {"method": "HIP events on the layer's stream around each step; ms_per_step = median",
+        "timing": {"method": "per step, the span of the library's timing-only HIP events (no system fence) "
+                             "on the layer's stream from before RMSNorm to after the combine; "
+                             "ms_per_step = median over the timed steps",
                    "mean_ms": head["mean_ms"], "min_ms": head["min_ms"], "max_ms": head["max_ms"],
                    "stage_sum_ms": head["stage_sum_ms"], "step_ms": head.pop("step_ms")},
         "stages_ms": head["stages_ms"],

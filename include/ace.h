@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define ACE_ABI_VERSION 3
+#define ACE_ABI_VERSION 4
 
 typedef enum {
   ACE_OK = 0,
@@ -180,12 +180,19 @@ ace_status ace_moe_forward_noalloc(const ace_moe_desc *desc, const void *x, cons
  *   5 combine.
  * ace_profile_end waits for the recorded events, writes the per-stage elapsed
  * time summed over the recorded calls (ms) into stage_ms[0..n_stages-1] and the
- * number of recorded calls into *n_calls, and destroys the events.  Only one
- * profile may be open per process; begin while open -> ACE_ERR_INVALID_ARG.
+ * number of recorded calls into *n_calls, optionally each call's stage times into
+ * call_stage_ms[c * n_stages + j] for the first max_calls calls (NULL: not
+ * written; the sum over j is that call's time from the start of its first stage
+ * to the end of its last; a stage that enqueued nothing for the call, such as the
+ * shared expert of a layer without one, records no event and counts zero), and
+ * destroys the events.  The events are created
+ * without a system-scope fence (timing only), so recording them does not flush
+ * the caches between stages.  Only one profile may be open per process; begin
+ * while open -> ACE_ERR_INVALID_ARG.
  */
 #define ACE_PROFILE_STAGES 6
 ace_status ace_profile_begin(int max_calls);
-ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls);
+ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls, double *call_stage_ms, int max_calls);
 
 /*
  * Budget-to-threshold mapping (App. C.1) on the device.  From the contribution

@@ -82,7 +82,8 @@ def lib() -> ctypes.CDLL:
         L.ace_profile_begin.argtypes = [ctypes.c_int]
         L.ace_profile_begin.restype = ctypes.c_int
         L.ace_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int,
-                                      ctypes.POINTER(ctypes.c_int)]
+                                      ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double),
+                                      ctypes.c_int]
         L.ace_profile_end.restype = ctypes.c_int
         L.ace_tables_workspace_size.argtypes = [ctypes.POINTER(Desc)]
         L.ace_tables_workspace_size.restype = ctypes.c_size_t
@@ -118,14 +119,21 @@ def profile_begin(max_calls: int) -> None:
         raise AceError(st, status_string(st))
 
 
-def profile_end() -> tuple[dict, int]:
-    """(summed ms per stage over the recorded calls, number of recorded calls)."""
-    arr = (ctypes.c_double * len(PROFILE_STAGES))()
+def profile_end(max_calls: int = 0):
+    """(summed ms per stage over the recorded calls, number of recorded calls); with
+    max_calls > 0 also a list of per-call {stage: ms} dicts for the first max_calls calls."""
+    ns = len(PROFILE_STAGES)
+    arr = (ctypes.c_double * ns)()
     n = ctypes.c_int(0)
-    st = int(lib().ace_profile_end(arr, len(PROFILE_STAGES), ctypes.byref(n)))
+    per = (ctypes.c_double * (ns * max_calls))() if max_calls > 0 else None
+    st = int(lib().ace_profile_end(arr, ns, ctypes.byref(n), per, int(max_calls)))
     if st != ACE_OK:
         raise AceError(st, status_string(st))
-    return dict(zip(PROFILE_STAGES, list(arr))), int(n.value)
+    tot = dict(zip(PROFILE_STAGES, list(arr)))
+    if max_calls <= 0:
+        return tot, int(n.value)
+    calls = [dict(zip(PROFILE_STAGES, per[c * ns:(c + 1) * ns])) for c in range(min(int(n.value), max_calls))]
+    return tot, int(n.value), calls
 
 
 def workspace_size(desc: Desc) -> int:

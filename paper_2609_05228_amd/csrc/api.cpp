@@ -9,6 +9,7 @@
 // caller workspace).
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <mutex>
@@ -152,19 +153,31 @@ struct Profile {
   int cap = 0;
   int used = 0;
   std::vector<hipEvent_t> ev;  // cap x (stages + 1)
+  std::vector<uint8_t> rec;    // cap x (stages + 1): event recorded (a stage that launches nothing records none)
 };
 Profile g_prof;
 constexpr int kStages = ACE_PROFILE_STAGES;
 
 // events of the next call, or null when no profile is open (or it is full)
-hipEvent_t *profile_slot() {
+struct ProfSlot {
+  hipEvent_t *ev = nullptr;
+  uint8_t *rec = nullptr;
+};
+ProfSlot profile_slot() {
   std::lock_guard<std::mutex> lk(g_prof.mu);
-  if (!g_prof.on || g_prof.used >= g_prof.cap) return nullptr;
-  return &g_prof.ev[static_cast<size_t>(g_prof.used++) * (kStages + 1)];
+  if (!g_prof.on || g_prof.used >= g_prof.cap) return {};
+  const size_t o = static_cast<size_t>(g_prof.used++) * (kStages + 1);
+  std::fill(g_prof.rec.begin() + o, g_prof.rec.begin() + o + kStages + 1, uint8_t{0});
+  return {&g_prof.ev[o], &g_prof.rec[o]};
 }
 
-void mark(hipEvent_t *slot, int i, hipStream_t s) {
-  if (slot) (void)hipEventRecord(slot[i], s);
+// event i after stage i-1; `launched` = false for a stage that enqueued nothing, whose
+// time then counts as zero (each record costs the stream a few microseconds)
+void mark(const ProfSlot &slot, int i, hipStream_t s, bool launched = true) {
+  if (slot.ev && (launched || i == 0 || i == kStages)) {
+    (void)hipEventRecord(slot.ev[i], s);
+    slot.rec[i] = 1;
+  }
 }
 
 // ---------------------------------------------------------------- static scratch
@@ -213,42 +226,57 @@ ace_status ace_profile_begin(int max_calls) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (g_prof.on || max_calls <= 0 || max_calls > 100000) return ACE_ERR_INVALID_ARG;
   g_prof.ev.assign(static_cast<size_t>(max_calls) * (kStages + 1), nullptr);
+  // timing-only events: no system-scope fence when recorded, so recording one does not
+  // write back and invalidate the caches between the stages it separates (a fenced
+  // record costs the stream several microseconds)
   for (auto &e : g_prof.ev)
-    if (hipEventCreate(&e) != hipSuccess) {
+    if (hipEventCreateWithFlags(&e, hipEventDisableSystemFence) != hipSuccess) {
       for (auto &x : g_prof.ev)
         if (x) (void)hipEventDestroy(x);
       g_prof.ev.clear();
       return ACE_ERR_HIP;
     }
+  g_prof.rec.assign(g_prof.ev.size(), uint8_t{0});
   g_prof.cap = max_calls;
   g_prof.used = 0;
   g_prof.on = true;
   return ACE_OK;
 }
 
-ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls) {
+ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls, double *call_stage_ms, int max_calls) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (!g_prof.on) return ACE_ERR_INVALID_ARG;
   ace_status st = ACE_OK;
   for (int j = 0; j < n_stages && stage_ms; ++j) stage_ms[j] = 0.0;
   for (int c = 0; c < g_prof.used && st == ACE_OK; ++c) {
     hipEvent_t *e = &g_prof.ev[static_cast<size_t>(c) * (kStages + 1)];
+    const uint8_t *rec = &g_prof.rec[static_cast<size_t>(c) * (kStages + 1)];
     if (hipEventSynchronize(e[kStages]) != hipSuccess) {
       st = ACE_ERR_HIP;
       break;
     }
-    for (int j = 0; j < kStages && j < n_stages; ++j) {
+    // stage j spans the last recorded event at or before j to event j+1; a stage whose
+    // end event was not recorded enqueued nothing and counts zero
+    int last = 0;
+    for (int j = 0; j < kStages; ++j) {
       float ms = 0.f;
-      if (hipEventElapsedTime(&ms, e[j], e[j + 1]) != hipSuccess) {
-        st = ACE_ERR_HIP;
-        break;
+      if (rec[j + 1]) {
+        if (hipEventElapsedTime(&ms, e[last], e[j + 1]) != hipSuccess) {
+          st = ACE_ERR_HIP;
+          break;
+        }
+        last = j + 1;
       }
-      if (stage_ms) stage_ms[j] += ms;
+      if (j < n_stages) {
+        if (stage_ms) stage_ms[j] += ms;
+        if (call_stage_ms && c < max_calls) call_stage_ms[static_cast<size_t>(c) * n_stages + j] = ms;
+      }
     }
   }
   if (n_calls) *n_calls = g_prof.used;
   for (auto &x : g_prof.ev) (void)hipEventDestroy(x);
   g_prof.ev.clear();
+  g_prof.rec.clear();
   g_prof.on = false;
   g_prof.cap = g_prof.used = 0;
   return st;
@@ -393,7 +421,7 @@ ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_w
   auto *tile_rows = static_cast<int32_t *>(at(L.tile_rows));
   auto *n_tiles = static_cast<int32_t *>(at(L.n_tiles));
 
-  hipEvent_t *prof = profile_slot();
+  const ProfSlot prof = profile_slot();
   mark(prof, 0, stream);
 
   ace::RouteArgs ra{};
@@ -458,7 +486,7 @@ ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_w
   const bool self_plan = L.skinny && L.G > 1;
   const bool planned = (L.ksplit > 0 && L.G == 1) || self_plan;
   if (!planned && ace::launch_plan(pa, stream) != hipSuccess) return ACE_ERR_HIP;
-  mark(prof, 2, stream);
+  mark(prof, 2, stream, !planned);
 
   ace::GemmArgs g{};
   g.act = at(L.xn);
@@ -558,7 +586,7 @@ ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_w
     }
     Ys = at(L.Ys);
   }
-  mark(prof, 5, stream);
+  mark(prof, 5, stream, d.n_shared == 1 && !shared_in_routed);
 
   ace::CombineArgs c{};
   c.Y = at(L.Y);
