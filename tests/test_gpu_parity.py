@@ -175,9 +175,11 @@ def test_prefill_4096_skip_disable(prefill):
     assert r["gpu"]["keep"].all()
 
 
-@pytest.mark.parametrize("B", [1, 8, 32, 64])
+@pytest.mark.parametrize("B", [1, 2, 3, 5, 8, 32, 64])
 def test_decode(prefill, B):
-    """Four seeded decode steps per batch size, every token's decisions and output."""
+    """Four seeded decode steps per batch size, every token's decisions and output
+    (B = 1-5 take K-split small-batch GEMMs with the SwiGLU split reduction, B = 8
+    unsplit gate/up, B = 32/64 the self-planned multi-chunk path)."""
     L, D, ag, ar, gold = prefill
     cfg = L["cfg"].with_(T=B)
     for step in range(4):
