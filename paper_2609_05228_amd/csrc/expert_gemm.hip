@@ -276,11 +276,6 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       for (int j = 0; j < NAM; ++j)
         if (j < na) dma16(asrc[j] + kofs(s), st + (wave + W * j) * kFragBytes);
     }
-    if (kt + SB - 1 < nk) {
-      const int s = kt + SB - 1;
-      const uint32_t st = ldsB + (s % SB) * P::BSZ;
-      issue_b(st, s);
-    }
     const uint8_t *sa = smemA + (kt % SA) * P::ASZ;
     const uint8_t *sb = smemB + (kt % SB) * P::BSZ;
 #pragma unroll
@@ -298,6 +293,14 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
 #pragma unroll
         for (int c = 0; c < 2 * CW; ++c)
           acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bf[c], acc[i][c], 0, 0, 0);
+      }
+      // the weight DMAs of stage kt + SB - 1 go out behind the first k half's
+      // MFMAs, so their issue (the memory pipeline's back-pressure) overlaps the
+      // matrix cores instead of delaying them; the issue order, and so every
+      // vmcnt count, is unchanged (A of a step, then its B)
+      if (h == 0 && kt + SB - 1 < nk) {
+        const int s = kt + SB - 1;
+        issue_b(ldsB + (s % SB) * P::BSZ, s);
       }
     }
   }

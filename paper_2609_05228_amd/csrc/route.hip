@@ -248,32 +248,58 @@ template <typename T, int NT> struct Depth {
   static constexpr int regs = (2 + NT) * static_cast<int>(sizeof(typename Oct<T>::raw)) / 4;
   static constexpr int fit = 160 / regs;
   static constexpr int value = fit >= 4 ? 4 : fit >= 1 ? fit : 1;
+  // register stages of the pipelined loop: what is left of 256 VGPRs after the
+  // accumulators (4 NT) and one stage's operands in flight to the MFMAs (4 NT + 48)
+  static constexpr int ring_fit = (256 - 8 * NT - 48) / regs;
+  static constexpr int ring = ring_fit >= 4 ? 4 : ring_fit;
 };
 
 // Blocks jfirst + step i (i < cnt, cnt = blocks below jend) of one wave, in
 // the order i = rot, rot + 1, ... (mod cnt): workgroups that start together
 // use different rotations so they do not all request the same router rows at
-// once.  Each round loads D blocks, then multiplies them; rounds past the end
-// load the last block again and zero its activations in the multiply, so
-// every load is unconditional.
+// once.  Sums run over the blocks in that fixed order.  When at least two
+// stages fit in registers, the blocks stream through a ring of D stages: block
+// i + D - 1 is requested before block i is multiplied, so D - 1 blocks' loads
+// stay in flight behind the MFMAs (the compiler's vmcnt waits follow the issue
+// order).  Otherwise each round loads D blocks, then multiplies them; rounds
+// past the end load the last block again and zero its activations in the
+// multiply, so every load is unconditional.
 template <typename T, int NT>
 __device__ __forceinline__ void accumulate_logits(const T *xrow, const T *gl, const T *wl, const int (&woff)[NT],
                                                   int jfirst, int jend, int step, int rot, f32x4_t (&acc)[NT],
                                                   float &ss) {
-  constexpr int D = Depth<T, NT>::value;
   const int cnt = jend > jfirst ? (jend - jfirst + step - 1) / step : 0;
   if (cnt == 0) return;
   rot %= cnt;
-  for (int i0 = 0; i0 < cnt; i0 += D) {
+  auto kof = [&](int i) {
+    int b = i + rot;
+    b = b >= cnt ? b - cnt : b;
+    return 32 * (jfirst + b * step);
+  };
+  if constexpr (Depth<T, NT>::ring >= 2) {
+    constexpr int D = Depth<T, NT>::ring;
     Stage<T, NT> st[D];
 #pragma unroll
-    for (int u = 0; u < D; ++u) {
-      int i = min(i0 + u, cnt - 1) + rot;
-      i = i >= cnt ? i - cnt : i;
-      load_stage<T, NT>(st[u], xrow, gl, wl, woff, 32 * (jfirst + i * step));
-    }
+    for (int u = 0; u < D - 1; ++u)
+      if (u < cnt) load_stage<T, NT>(st[u], xrow, gl, wl, woff, kof(u));
+    for (int i0 = 0; i0 < cnt; i0 += D) {
 #pragma unroll
-    for (int u = 0; u < D; ++u) mma_stage<NT>(st[u], acc, ss, i0 + u < cnt);
+      for (int u = 0; u < D; ++u) {
+        const int i = i0 + u;
+        if (i >= cnt) break;
+        if (i + D - 1 < cnt) load_stage<T, NT>(st[(u + D - 1) % D], xrow, gl, wl, woff, kof(i + D - 1));
+        mma_stage<NT>(st[u], acc, ss, true);
+      }
+    }
+  } else {
+    constexpr int D = Depth<T, NT>::value;
+    for (int i0 = 0; i0 < cnt; i0 += D) {
+      Stage<T, NT> st[D];
+#pragma unroll
+      for (int u = 0; u < D; ++u) load_stage<T, NT>(st[u], xrow, gl, wl, woff, kof(min(i0 + u, cnt - 1)));
+#pragma unroll
+      for (int u = 0; u < D; ++u) mma_stage<NT>(st[u], acc, ss, i0 + u < cnt);
+    }
   }
 }
 
@@ -658,29 +684,35 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
 // Batches of more than 256 chunks (bf16): one workgroup of 8 waves per pair of
 // chunks (32 tokens).  Each router-row fragment a wave loads feeds the MFMAs of
 // both 16-token tiles, so every CU streams W_r once per two chunks, and the
-// grid is one round of workgroups instead of two.  Same products and the same
-// kind of fixed summation as route_kernel (blocks in order within a wave; then
-// waves w and w + 4 first, those four sums in order); then selection (waves
-// 0-3: the first chunk's tokens, waves 4-7: the second's), x_in for the 32
-// rows, and per-chunk ranks and counts.
+// grid is one round of workgroups instead of two.  The waves split the experts
+// in two halves (NT >= 2) and K in four groups: wave w multiplies expert tiles
+// (w % 2) NT/2 .. and K blocks w/2, w/2 + 4, ..., so its accumulators and a
+// register stage stay small enough for a ring of stages (block i + D - 1 is
+// requested before block i is multiplied).  Fixed summation: blocks in order
+// within a wave, then the four K groups in order; then selection (waves 0-3:
+// the first chunk's tokens, waves 4-7: the second's), x_in for the 32 rows, and
+// per-chunk ranks and counts.
 constexpr int kPairWaves = 8;
-template <int NT> struct PairStage {
-  uint4 x[2], g, w[NT];
+template <int NTW> struct PairStage {
+  uint4 x[2], g, w[NTW];
 };
-// K blocks in flight per wave within 2 waves per SIMD: accumulators 8 NT, a stage
-// 4 (3 + NT), about 40 more
-template <int NT> struct PairDepth {
-  static constexpr int fit = (256 - 8 * NT - 40) / ((3 + NT) * 4);
-  static constexpr int value = fit >= 3 ? 3 : fit >= 1 ? fit : 1;
+// register stages per wave within 2 waves per SIMD: accumulators 8 NTW, the
+// operands of one stage on their way to the MFMAs 4 (NTW + 2), about 40 more
+template <int NTW> struct PairDepth {
+  static constexpr int fit = (256 - 8 * NTW - 4 * (NTW + 2) - 40) / ((3 + NTW) * 4);
+  static constexpr int value = fit >= 4 ? 4 : fit >= 1 ? fit : 1;
 };
 
 template <int NT>
 __global__ __launch_bounds__(512) void route_pair_kernel(RouteArgs a) {
   constexpr int NP = NT * 16, TOK = 2 * kTok;
-  constexpr int D = PairDepth<NT>::value;
+  constexpr int EH = NT >= 2 ? 2 : 1;       // expert groups
+  constexpr int NTW = NT / EH;              // expert tiles per wave
+  constexpr int KG = kPairWaves / EH;       // K groups
+  constexpr int D = PairDepth<NTW>::value;
   static_assert(512 % NP == 0, "a thread meets one expert column in the logits reduction");
-  __shared__ float zred[kPairWaves / 2][TOK][NP + 1];  // waves w and w + 4 share slot w
-  __shared__ float ssred[kPairWaves][TOK];
+  __shared__ float zred[KG][TOK][NP + 1];   // K group kg's partial logits (all experts)
+  __shared__ float ssred[KG][TOK];
   __shared__ float rstd_s[TOK];
   __shared__ uint32_t emask[2][NP];
   __shared__ float a_gsp_s[NP], a_rcr_s[NP];
@@ -700,109 +732,104 @@ __global__ __launch_bounds__(512) void route_pair_kernel(RouteArgs a) {
   }
   const float bias = (a.b_router && (tid % NP) < N) ? a.b_router[tid % NP] : 0.f;
 
-  // ---- 1. logits of both token tiles: wave w takes K blocks w, w + 4, ...
+  // ---- 1. logits of both token tiles
   {
+    const int eh = wave % EH, kg = wave / EH;
     const int lrow = lane >> 2, lchunk = lane & 3;  // row-major fragment loads
     const bf16_t *xrow[2];
 #pragma unroll
     for (int c = 0; c < 2; ++c) xrow[c] = x + static_cast<size_t>(min(t0 + 16 * c + lrow, nt - 1)) * d + lchunk * 8;
     const bf16_t *gl = gamma + grp * 8;
     const bf16_t *wl = static_cast<const bf16_t *>(a.w_router) + lchunk * 8;
-    int woff[NT];
+    int woff[NTW];
 #pragma unroll
-    for (int f = 0; f < NT; ++f) woff[f] = min(16 * f + lrow, N - 1) * d;
-    f32x4_t acc[2][NT];
+    for (int f = 0; f < NTW; ++f) woff[f] = min(16 * (eh * NTW + f) + lrow, N - 1) * d;
+    f32x4_t acc[2][NTW];
     float ss[2] = {0.f, 0.f};
 #pragma unroll
     for (int c = 0; c < 2; ++c)
 #pragma unroll
-      for (int f = 0; f < NT; ++f) acc[c][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+      for (int f = 0; f < NTW; ++f) acc[c][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const int nb = d >> 5;
-    const int cnt = nb > wave ? (nb - wave + kPairWaves - 1) / kPairWaves : 0;
+    const int cnt = nb > kg ? (nb - kg + KG - 1) / KG : 0;
     const int rot = cnt > 0 ? static_cast<int>((blockIdx.x >> 3) % cnt) : 0;
-    for (int i0 = 0; i0 < cnt; i0 += D) {
-      PairStage<NT> st[D];
+    auto load = [&](PairStage<NTW> &st, int i) {
+      int b = i + rot;
+      b = b >= cnt ? b - cnt : b;
+      const int k = 32 * (kg + b * KG);
 #pragma unroll
-      for (int u = 0; u < D; ++u) {
-        if (u > 0 && i0 + u >= cnt) break;
-        int i = i0 + u + rot;
-        i = i >= cnt ? i - cnt : i;
-        const int k = 32 * (wave + i * kPairWaves);
+      for (int c = 0; c < 2; ++c) st.x[c] = *reinterpret_cast<const uint4 *>(xrow[c] + k);
+      st.g = *reinterpret_cast<const uint4 *>(gl + k);
 #pragma unroll
-        for (int c = 0; c < 2; ++c) st[u].x[c] = *reinterpret_cast<const uint4 *>(xrow[c] + k);
-        st[u].g = *reinterpret_cast<const uint4 *>(gl + k);
+      for (int f = 0; f < NTW; ++f) st.w[f] = *reinterpret_cast<const uint4 *>(wl + woff[f] + k);
+    };
+    auto mma = [&](const PairStage<NTW> &st) {
+      float gv[8];
+      Oct<bf16_t>::cvt(st.g, gv);
 #pragma unroll
-        for (int f = 0; f < NT; ++f) st[u].w[f] = *reinterpret_cast<const uint4 *>(wl + woff[f] + k);
-      }
+      for (int c = 0; c < 2; ++c) {
+        float xv[8];
+        Oct<bf16_t>::cvt(to_operand_order(st.x[c]), xv);
+        uint32_t hi[4], lo[4];
 #pragma unroll
-      for (int u = 0; u < D; ++u) {
-        if (u > 0 && i0 + u >= cnt) break;
-        float gv[8];
-        Oct<bf16_t>::cvt(st[u].g, gv);
+        for (int q = 0; q < 4; ++q) {
+          uint32_t h[2], l[2];
 #pragma unroll
-        for (int c = 0; c < 2; ++c) {
-          float xv[8];
-          Oct<bf16_t>::cvt(to_operand_order(st[u].x[c]), xv);
-          uint32_t hi[4], lo[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            uint32_t h[2], l[2];
-#pragma unroll
-            for (int v = 0; v < 2; ++v) {
-              const float xe = xv[2 * q + v];
-              ss[c] = fmaf(xe, xe, ss[c]);
-              const float pr = xe * gv[2 * q + v];  // exact: two 8-bit significands
-              const uint32_t pb = __float_as_uint(pr) & 0xFFFF0000u;
-              h[v] = pb;
-              l[v] = __float_as_uint(pr - __uint_as_float(pb));  // exact, <= 8 significant bits
-            }
-            hi[q] = (h[0] >> 16) | h[1];
-            lo[q] = (l[0] >> 16) | (l[1] & 0xFFFF0000u);
+          for (int v = 0; v < 2; ++v) {
+            const float xe = xv[2 * q + v];
+            ss[c] = fmaf(xe, xe, ss[c]);
+            const float pr = xe * gv[2 * q + v];  // exact: two 8-bit significands
+            const uint32_t pb = __float_as_uint(pr) & 0xFFFF0000u;
+            h[v] = pb;
+            l[v] = __float_as_uint(pr - __uint_as_float(pb));  // exact, <= 8 significant bits
           }
-          const bf16x8_t ahi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
-          const bf16x8_t alo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
+          hi[q] = (h[0] >> 16) | h[1];
+          lo[q] = (l[0] >> 16) | (l[1] & 0xFFFF0000u);
+        }
+        const bf16x8_t ahi = __builtin_bit_cast(bf16x8_t, make_uint4(hi[0], hi[1], hi[2], hi[3]));
+        const bf16x8_t alo = __builtin_bit_cast(bf16x8_t, make_uint4(lo[0], lo[1], lo[2], lo[3]));
 #pragma unroll
-          for (int f = 0; f < NT; ++f) {
-            const bf16x8_t w = __builtin_bit_cast(bf16x8_t, to_operand_order(st[u].w[f]));
-            acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, w, acc[c][f], 0, 0, 0);
-            acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, w, acc[c][f], 0, 0, 0);
-          }
+        for (int f = 0; f < NTW; ++f) {
+          const bf16x8_t w = __builtin_bit_cast(bf16x8_t, to_operand_order(st.w[f]));
+          acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ahi, w, acc[c][f], 0, 0, 0);
+          acc[c][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(alo, w, acc[c][f], 0, 0, 0);
         }
       }
+    };
+    PairStage<NTW> st[D];
+#pragma unroll
+    for (int u = 0; u < D - 1; ++u)
+      if (u < cnt) load(st[u], u);
+    for (int i0 = 0; i0 < cnt; i0 += D) {
+#pragma unroll
+      for (int u = 0; u < D; ++u) {
+        const int i = i0 + u;
+        if (i >= cnt) break;
+        if (i + D - 1 < cnt) load(st[(u + D - 1) % D], i + D - 1);
+        mma(st[u]);
+      }
     }
-    // D[row = token 4 grp + i][col = expert 16 f + r16] of each token tile:
-    // waves 0-3 store theirs, then waves 4-7 add theirs to slot wave - 4
-    const int slot = wave & 3;
+    // D[row = token 4 grp + i][col = expert 16 f + r16] of each token tile into
+    // the K group's slot; the sums of squares once per K group (expert group 0)
 #pragma unroll
     for (int c = 0; c < 2; ++c) {
       float v = ss[c];
       v += __shfl_xor(v, 16);
       v += __shfl_xor(v, 32);
-      if (grp == 0) ssred[wave][16 * c + r16] = v;
+      if (eh == 0 && grp == 0) ssred[kg][16 * c + r16] = v;
     }
-    if (wave < 4) {
 #pragma unroll
-      for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < 2; ++c)
 #pragma unroll
-        for (int f = 0; f < NT; ++f)
+      for (int f = 0; f < NTW; ++f)
 #pragma unroll
-          for (int i = 0; i < 4; ++i) zred[slot][16 * c + grp * 4 + i][16 * f + r16] = acc[c][f][i];
-    }
-    __syncthreads();
-    if (wave >= 4) {
-#pragma unroll
-      for (int c = 0; c < 2; ++c)
-#pragma unroll
-        for (int f = 0; f < NT; ++f)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) zred[slot][16 * c + grp * 4 + i][16 * f + r16] += acc[c][f][i];
-    }
+        for (int i = 0; i < 4; ++i) zred[kg][16 * c + grp * 4 + i][16 * (eh * NTW + f) + r16] = acc[c][f][i];
   }
   __syncthreads();
   if (tid < TOK) {
     float ssum = 0.f;
 #pragma unroll
-    for (int w = 0; w < kPairWaves; ++w) ssum += ssred[w][tid];
+    for (int w = 0; w < KG; ++w) ssum += ssred[w][tid];
     rstd_s[tid] = 1.0f / sqrtf(ssum / static_cast<float>(d) + a.rms_eps);
   }
   __syncthreads();
@@ -811,7 +838,7 @@ __global__ __launch_bounds__(512) void route_pair_kernel(RouteArgs a) {
     const int e = idx - tl * NP;
     float z = 0.f;
 #pragma unroll
-    for (int w = 0; w < kPairWaves / 2; ++w) z += zred[w][tl][e];
+    for (int w = 0; w < KG; ++w) z += zred[w][tl][e];
     zred[0][tl][e] = z * rstd_s[tl] + bias;
   }
   __syncthreads();
