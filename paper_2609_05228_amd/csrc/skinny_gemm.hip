@@ -11,9 +11,11 @@
 //  * it reads MFMA fragments back from the ring and multiplies them with
 //    v_mfma_f32_16x16x32_bf16;
 //  * with one K split the epilogue writes H (SwiGLU applied) or Y in bf16;
-//    with several, it writes fp32 partial sums, which swiglu_reduce_kernel (for
-//    H) and the combine kernel (for Y) add in split order, so the result does
-//    not depend on scheduling;
+//    gate/up with several splits runs the splits of one 16-feature block as the
+//    waves of one workgroup, which add their fp32 partial sums in split order
+//    through LDS and write H (no reduction kernel); down with several splits
+//    writes fp32 partial sums, which the combine kernel adds in split order, so
+//    results do not depend on scheduling;
 //  * batches of 2-4 router chunks need no plan kernel: each gate/up wave derives
 //    its tile and the tokens of its rows from the router's per-chunk counts and
 //    the routing (self_tile), and the gate/up launch writes the plan outputs and
@@ -181,9 +183,13 @@ template <int AU> struct SkinnyRing {
 // whether a ring holds two stages of a 32-row (two-block) item
 constexpr bool kSkinnyTwoBlocks = kSkinnyRingBytes / ((4 + 4) * kUnitBytes) >= 2;
 
+// red != null (gate/up, K splits as the waves of one workgroup, wave index =
+// split): the partial sums go through red (LDS, over the workgroup's rings) and
+// wave 0 adds them in split order and writes H; every wave of the workgroup
+// calls this with the same tile rows.
 template <bool GATEUP, int MB, int AU>
 __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo &ti, int nb, int s, int rot,
-                                            bool once, int tok, int rbase, uint8_t *ring) {
+                                            bool once, int tok, int rbase, uint8_t *ring, f32x4_t *red) {
   static_assert(AU == 2 * MB || (MB == 1 && AU == 1), "activation units cover the row blocks");
   using R = SkinnyRing<AU>;
   constexpr int P = R::P, NU = R::NU;
@@ -278,6 +284,36 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
     }
   }
 
+  if (GATEUP && red != nullptr) {
+    // every wave's last wait covered all its DMAs, so after the barrier no ring
+    // is written any more and red may overlay them
+    __syncthreads();
+    const int w = threadIdx.x >> 6;
+#pragma unroll
+    for (int mi = 0; mi < MB; ++mi)
+#pragma unroll
+      for (int cb = 0; cb < 2; ++cb) red[((w * MB + mi) * 2 + cb) * 64 + lane] = acc[mi][cb];
+    __syncthreads();
+    if (w == 0) {
+#pragma unroll
+      for (int mi = 0; mi < MB; ++mi)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          // the splits in order from zero, as a separate reduction would add them
+          float gs = 0.f, us = 0.f;
+          for (int sp = 0; sp < sa.splits; ++sp) {
+            gs += red[((sp * MB + mi) * 2 + 0) * 64 + lane][q];
+            us += red[((sp * MB + mi) * 2 + 1) * 64 + lane][q];
+          }
+          const int row = mi * 16 + 4 * g + q;
+          if (row < ti.rows)
+            static_cast<bf16_t *>(a.out)[static_cast<size_t>(ti.row0 + row) * a.m + nb * 16 + r16] =
+                f32_to_bf16(silu_for_bf16(gs) * us);
+        }
+    }
+    __syncthreads();  // red is overwritten by the next pass's DMAs
+    return;
+  }
   // epilogue: lane holds column r16 of each block, rows 4*g + q
 #pragma unroll
   for (int mi = 0; mi < MB; ++mi)
@@ -310,19 +346,32 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
     }
 }
 
-// one wave per work item; item = ((grp * splits) + s) * nN + nb
-template <bool GATEUP>
-__global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(SkinnyArgs sa) {
-  __shared__ __align__(16) uint8_t smem[kSkinnyWavesPerGroup * kSkinnyRingBytes];
+// WGS = 0: one wave per work item, item = ((grp * splits) + s) * nN + nb, four
+// independent waves per workgroup.  WGS = splits (gate/up): workgroup
+// grp * nN + nb, wave s; the waves add their partial sums through LDS.
+template <bool GATEUP, int WGS>
+__global__ __launch_bounds__((WGS ? WGS : kSkinnyWavesPerGroup) * 64) void skinny_gemm_kernel(SkinnyArgs sa) {
+  constexpr int NW = WGS ? WGS : kSkinnyWavesPerGroup;
+  static_assert(!WGS || GATEUP, "workgroup reduction: gate/up only");
+  static_assert(!WGS || 2 * 2 * 64 * 16 <= kSkinnyRingBytes, "partials of a wave fit its ring");
+  __shared__ __align__(16) uint8_t smem[NW * kSkinnyRingBytes];
   const GemmArgs &a = sa.g;
   const int nN = GATEUP ? a.m / 16 : a.d / 32;
   const int wave = threadIdx.x >> 6;
   uint8_t *ring = smem + wave * kSkinnyRingBytes;
-  const long item = static_cast<long>(blockIdx.x) * kSkinnyWavesPerGroup + wave;
-  const int nb = static_cast<int>(item % nN);
-  const long rest = item / nN;
-  const int s = static_cast<int>(rest % sa.splits);
-  const int grp = static_cast<int>(rest / sa.splits);
+  f32x4_t *red = WGS ? reinterpret_cast<f32x4_t *>(smem) : nullptr;
+  const long item = static_cast<long>(blockIdx.x) * NW + wave;
+  int nb, s, grp;
+  if constexpr (WGS > 0) {
+    nb = static_cast<int>(blockIdx.x % nN);
+    grp = static_cast<int>(blockIdx.x / nN);
+    s = wave;
+  } else {
+    nb = static_cast<int>(item % nN);
+    const long rest = item / nN;
+    s = static_cast<int>(rest % sa.splits);
+    grp = static_cast<int>(rest / sa.splits);
+  }
   if (grp >= a.max_groups) return;
   int tok = 0;
   const TileInfo ti = (GATEUP && sa.self_plan) ? self_tile(sa, grp, nb == 0 && s == 0, item == 0, &tok)
@@ -331,14 +380,14 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
   const int blocks = (ti.rows + 15) >> 4;
   const int rot = static_cast<int>(item & 0x7fffffff);
   if (ti.rows <= 8) {
-    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, rot, true, tok, 0, ring);
+    skinny_item<GATEUP, 1, 1>(sa, ti, nb, s, rot, true, tok, 0, ring, red);
   } else if (blocks <= 1 || !kSkinnyTwoBlocks) {
     // 16 rows per pass (more than 16 rows re-read the weights, mostly from L2)
     for (int r = 0; r < ti.rows; r += 16) {
       TileInfo part = ti;
       part.row0 = ti.row0 + r;
       part.rows = min(16, ti.rows - r);
-      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, rot, ti.rows <= 16, tok, r, ring);
+      skinny_item<GATEUP, 1, 2>(sa, part, nb, s, rot, ti.rows <= 16, tok, r, ring, red);
     }
   } else if constexpr (kSkinnyTwoBlocks) {
     // 32 rows per pass
@@ -346,7 +395,7 @@ __global__ __launch_bounds__(kSkinnyWavesPerGroup * 64) void skinny_gemm_kernel(
       TileInfo part = ti;
       part.row0 = ti.row0 + r;
       part.rows = min(32, ti.rows - r);
-      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, rot, ti.rows <= 32, tok, r, ring);
+      skinny_item<GATEUP, 2, 4>(sa, part, nb, s, rot, ti.rows <= 32, tok, r, ring, red);
     }
   }
 }
@@ -392,15 +441,24 @@ hipError_t launch_skinny(const SkinnyArgs &sa, bool gateup, const int32_t *n_row
   const dim3 grid(static_cast<unsigned>((items + kSkinnyWavesPerGroup - 1) / kSkinnyWavesPerGroup));
   if (gateup) {
     if (sa.splits > kMaxGateUpSplits) return hipErrorInvalidValue;
-    skinny_gemm_kernel<true><<<grid, kSkinnyWavesPerGroup * 64, 0, stream>>>(sa);
-    if (sa.splits > 1) {
-      const size_t total = static_cast<size_t>(sa.rows_cap) * a.m;
-      size_t blocks = (total + 255) / 256;
-      if (blocks > 2048) blocks = 2048;
-      swiglu_reduce_kernel<<<dim3(static_cast<unsigned>(blocks)), 256, 0, stream>>>(sa, n_rows);
+    // several K splits: the splits of a 16-feature block are one workgroup's waves
+    const dim3 wg_grid(static_cast<unsigned>(static_cast<long>(a.max_groups) * nN));
+    switch (sa.splits) {
+      case 1: skinny_gemm_kernel<true, 0><<<grid, kSkinnyWavesPerGroup * 64, 0, stream>>>(sa); break;
+      case 2: skinny_gemm_kernel<true, 2><<<wg_grid, 2 * 64, 0, stream>>>(sa); break;
+      case 4: skinny_gemm_kernel<true, 4><<<wg_grid, 4 * 64, 0, stream>>>(sa); break;
+      case 8: skinny_gemm_kernel<true, 8><<<wg_grid, 8 * 64, 0, stream>>>(sa); break;
+      default: {
+        // other split counts: partial sums, then the reduction kernel
+        skinny_gemm_kernel<true, 0><<<grid, kSkinnyWavesPerGroup * 64, 0, stream>>>(sa);
+        const size_t total = static_cast<size_t>(sa.rows_cap) * a.m;
+        size_t blocks = (total + 255) / 256;
+        if (blocks > 2048) blocks = 2048;
+        swiglu_reduce_kernel<<<dim3(static_cast<unsigned>(blocks)), 256, 0, stream>>>(sa, n_rows);
+      }
     }
   } else {
-    skinny_gemm_kernel<false><<<grid, kSkinnyWavesPerGroup * 64, 0, stream>>>(sa);
+    skinny_gemm_kernel<false, 0><<<grid, kSkinnyWavesPerGroup * 64, 0, stream>>>(sa);
   }
   return hipGetLastError();
 }
