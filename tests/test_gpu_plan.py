@@ -23,6 +23,8 @@ CASES = [
     (8192, 256, 2),    # one kernel at the 128 KB limit (512 chunks x 256 experts)
     (8208, 256, 2),    # two kernels: one chunk past it
     (4097, 128, 8),    # one kernel, ragged last chunk (one token)
+    (4200, 16, 2),     # router: chunk pairs with one 16-expert tile (all experts per wave)
+    (4200, 30, 4),     # router: chunk pairs with two expert tiles (one per wave); two plan kernels
 ]
 
 
