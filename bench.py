@@ -57,13 +57,14 @@ STAGE_KERNEL = {"gateup": ("grouped_gemm_bf16_kernel<true, 8, 8>", "expert_gemm.
 
 
 def source_digest(src: str) -> str:
-    """First 16 hex digits of sha256 over a kernel's source file and the
-    shared headers it includes: the key that ties a traffic record to the code."""
+    """First 16 hex digits of sha256 over a kernel's source file and every shared
+    header of the sources: the key that ties a traffic record to the code."""
     import hashlib
 
+    csrc = os.path.join(ROOT, "paper_2609_05228_amd", "csrc")
     h = hashlib.sha256()
-    for f in (src, "ace_internal.h"):
-        h.update(open(os.path.join(ROOT, "paper_2609_05228_amd", "csrc", f), "rb").read())
+    for f in [src] + sorted(n for n in os.listdir(csrc) if n.endswith(".h")):
+        h.update(open(os.path.join(csrc, f), "rb").read())
     return h.hexdigest()[:16]
 
 

@@ -35,6 +35,7 @@
 // Launch order is XCD-aware: workgroups are dealt to the 8 XCDs round-robin, so
 // block b runs on XCD b % 8; the N tiles of one M tile are mapped to one XCD so
 // the activation rows they share stay in that XCD's L2.
+#include "gemm_pipe.h"
 #include "lds_dma.h"
 
 namespace ace {
@@ -42,7 +43,8 @@ namespace ace {
 namespace {
 
 constexpr int kFragBytes = kUnitBytes;  // one staged unit (8 rows x 64 bf16, or 16 rows x 32)
-constexpr int kLdsBytes = 160 * 1024;
+constexpr int kLdsBytes = kPipeLdsBytes;
+static_assert(kFragBytes == kPipeUnitBytes, "one DMA unit per fragment");
 
 struct TileInfo {
   int e, row0, rows;
@@ -96,62 +98,8 @@ constexpr int kGemmWaves = 8;  // waves per workgroup (two per SIMD)
 // one with deeper rings: the stream rate, not the bytes in flight, is the limit.
 template <int CG> constexpr int stage_halves() { return 2; }
 
-// Pipeline geometry for a tile of MB 16-row blocks (MB a multiple of 4), CG
-// column groups (gate/up: 16 features each, a gate and an up block; down: 32
-// output columns, two blocks) and KH 32-wide k halves per stage (BK = 32 KH).
-// A (activation rows, mostly L2 hits) and B (expert weights, streamed from HBM)
-// have their own LDS rings.  A stage of A holds MB*KH fragments spread over the
-// 8 waves (a wave stages na <= NA_MAX of them); a stage of B holds 2*CG*KH
-// fragments, NB per wave.
-template <int MB, int CG, int KH, int W> struct Pipe {
-  static constexpr int BK = 32 * KH;
-  static constexpr int FA = MB * KH;                      // A fragments per stage
-  static constexpr int NA_MAX = (FA + W - 1) / W;
-  static constexpr int NB = 2 * CG * KH / W;              // B DMAs per wave per stage
-  static constexpr int ASZ = FA * kFragBytes;
-  static constexpr int BSZ = 2 * CG * KH * kFragBytes;
-  static constexpr int SA = KH == 2 ? ((MB >= 16 || (CG >= 8 && MB >= 8)) ? 2 : MB >= 8 ? 3 : 4) : 4;
-  static constexpr int SB0 = (kLdsBytes - SA * ASZ) / BSZ;
-  static constexpr int SBMAX = KH == 2 ? 8 : 10;
-  static constexpr int SB = SB0 > SBMAX ? SBMAX : SB0;
-  static_assert(2 * CG * KH % W == 0, "B fragments must spread evenly over the waves");
-  static_assert(SB >= 2 && SA >= 2, "ring too shallow");
-  static_assert(SA * ASZ + SB * BSZ <= kLdsBytes, "rings exceed LDS");
-  static_assert((SA - 1) * NA_MAX + (SB - 1) * NB + NA_MAX + NB <= 63, "outstanding DMAs exceed the wait table");
-};
-
-// This wave's DMA issue sequence: a prologue of B stages 0..PB-1 then A stages
-// 0..PA-1 (PB = min(SB-1, nk), PA = min(SA-1, nk)); then iteration j issues
-// A(j+SA-1) and then B(j+SB-1), each only if it exists.  cum_ops(j) = DMAs
-// issued before iteration j.
-template <class P>
-__device__ __forceinline__ int cum_ops(int j, int nk, int na) {
-  const int PB = min(P::SB - 1, nk), PA = min(P::SA - 1, nk);
-  return PB * P::NB + PA * na + max(0, min(j, nk - P::SA + 1)) * na + max(0, min(j, nk - P::SB + 1)) * P::NB;
-}
-
-// DMAs that may still be outstanding at the wait before stage kt's compute:
-// everything issued after the later of A(kt) and B(kt) (vmcnt completes in
-// issue order).  na = this wave's A DMAs per stage.
-template <class P>
-__device__ __forceinline__ int pending_ok(int kt, int nk, int na) {
-  const int PB = min(P::SB - 1, nk), PA = min(P::SA - 1, nk);
-  int end_a, end_b;
-  if (na == 0) {
-    end_a = 0;  // this wave stages no A fragments
-  } else if (kt < PA) {
-    end_a = PB * P::NB + (kt + 1) * na;
-  } else {
-    end_a = cum_ops<P>(kt - P::SA + 1, nk, na) + na;
-  }
-  if (kt < PB) {
-    end_b = (kt + 1) * P::NB;
-  } else {
-    const int i = kt - P::SB + 1;
-    end_b = cum_ops<P>(i, nk, na) + (i + P::SA - 1 < nk ? na : 0) + P::NB;
-  }
-  return cum_ops<P>(kt, nk, na) - max(end_a, end_b);
-}
+// Pipe, cum_ops and pending_ok (gemm_pipe.h): ring depths per tile shape and
+// the exact wait counts of a wave's DMA issue sequence.
 
 // One M tile x one N tile with MB 16-row blocks, CG column groups and KH = 2
 // k halves per stage (64-wide stages: 128 bytes of every row).  One DMA
