@@ -111,6 +111,7 @@ struct PlanArgs {
   int32_t *tile_row0;                // [max_tiles]
   int32_t *tile_rows;                // [max_tiles]
   int32_t *n_tiles;                  // [1]
+  int32_t *tile_order;               // [max_tiles] or null: the gate/up launch's tile order (see plan_kernel)
   int T, k, N, G;
 };
 
@@ -125,6 +126,7 @@ struct GemmArgs {
   const void *w1;         // gate/up: w_up   [E, m, d]; down: unused
   void *out;              // gate/up: H [rows, m]; down: Y [rows, d]
   const int32_t *tile_expert, *tile_row0, *tile_rows, *n_tiles;
+  const int32_t *tile_order;  // null: tiles in list order; else grid tile g is list tile tile_order[g]
   int dense_rows;         // > 0: dense single-group mode with this many rows
   int max_groups;         // upper bound of M tiles (grid sizing)
   int d, m;               // hidden and intermediate sizes of this GEMM's expert(s)
@@ -179,6 +181,8 @@ hipError_t launch_down(const GemmArgs &a, bool bf16, hipStream_t stream);
 hipError_t launch_combine(const CombineArgs &a, bool bf16, hipStream_t stream);
 // gate/up (gateup = true; reduces K-split partials into H when splits > 1, with
 // n_rows = device count of rows in routed mode) or down
+// whether launch_plan writes PlanArgs::tile_order for these sizes (the one-kernel plan)
+bool plan_writes_order(const PlanArgs &a);
 hipError_t launch_skinny(const SkinnyArgs &a, bool gateup, const int32_t *n_rows, hipStream_t stream);
 
 // Offline GSP / RCR tables (Alg. 2, Alg. 3) in fp64

@@ -39,7 +39,7 @@ int pick_splits(long items, int K) {
 
 struct Layout {
   size_t xn, zpart, sspart, local_rank, chunk_count, chunk_base, slot_row, gates, counts, offsets, perm;
-  size_t tile_e, tile_r0, tile_rows, n_tiles, H, Y, Hs, Ys, part_g, part_u, part_y, total;
+  size_t tile_e, tile_r0, tile_rows, tile_ord, n_tiles, H, Y, Hs, Ys, part_g, part_u, part_y, total;
   int G, max_groups, dense_groups;
   bool skinny;          // small-batch path (bf16, T <= kSkinnyMaxT)
   int splits_gu, splits_dn;
@@ -90,6 +90,7 @@ Layout layout_for(const ace_moe_desc &d) {
   L.tile_e = take(static_cast<size_t>(L.max_groups) * 4);
   L.tile_r0 = take(static_cast<size_t>(L.max_groups) * 4);
   L.tile_rows = take(static_cast<size_t>(L.max_groups) * 4);
+  L.tile_ord = take(static_cast<size_t>(L.max_groups) * 4);
   L.n_tiles = take(4);
   L.H = take(slots * m * esz);
   L.Y = take(slots * dd * esz);
@@ -419,6 +420,7 @@ ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_w
   auto *tile_e = static_cast<int32_t *>(at(L.tile_e));
   auto *tile_r0 = static_cast<int32_t *>(at(L.tile_r0));
   auto *tile_rows = static_cast<int32_t *>(at(L.tile_rows));
+  auto *tile_ord = static_cast<int32_t *>(at(L.tile_ord));
   auto *n_tiles = static_cast<int32_t *>(at(L.n_tiles));
 
   const ProfSlot prof = profile_slot();
@@ -476,6 +478,7 @@ ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_w
   pa.tile_expert = tile_e;
   pa.tile_row0 = tile_r0;
   pa.tile_rows = tile_rows;
+  pa.tile_order = tile_ord;
   pa.n_tiles = n_tiles;
   pa.T = d.T;
   pa.k = d.k;
@@ -498,11 +501,14 @@ ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_w
   g.tile_row0 = tile_r0;
   g.tile_rows = tile_rows;
   g.n_tiles = n_tiles;
+  // the gate/up launch takes the plan kernel's tile order when it wrote one
+  g.tile_order = (!planned && ace::plan_writes_order(pa)) ? tile_ord : nullptr;
   g.dense_rows = 0;
   g.max_groups = L.max_groups;
   g.d = d.d;
   g.m = d.m;
   ace::GemmArgs gd = g;
+  gd.tile_order = nullptr;  // the down launch keeps list order
   gd.act = at(L.H);
   gd.perm = nullptr;
   gd.w0 = w->w_down;

@@ -135,6 +135,9 @@ __global__ __launch_bounds__(128) void scatter_kernel(PlanArgs a) {
 }
 
 constexpr int kPlanMaxBytes = 128 * 1024;  // count matrix size up to which one kernel plans
+#ifndef ACE_PLAN_LPT
+#define ACE_PLAN_LPT 1
+#endif
 
 // One kernel for the whole plan when the [G, N] count matrix is small: every
 // chunk workgroup reads the whole matrix (L2-resident after the first reads) and
@@ -238,6 +241,28 @@ __global__ __launch_bounds__(256) void plan_kernel(PlanArgs a) {
     for (int e = tid; e <= N; e += 256) a.offsets[e] = off[e];
     if (tid == 0) a.n_tiles[0] = toff[N];
   }
+  // The gate/up launch's tile order.  When every expert fits one M tile, longest
+  // first (rows descending, then expert id): its grid takes tiles in this order,
+  // so the longest tiles start first and the last round of workgroups holds the
+  // short ones.  Otherwise list order, which keeps an expert's tiles adjacent
+  // (their grid neighbours share its weights in L2).  The down launch keeps list
+  // order: there, concurrent workgroups then read and write neighbouring H and Y
+  // rows (longest first measured slower for it).  Workgroup g places experts g,
+  // g + G, ...: the position is the count of experts with more rows, or as many
+  // rows and a lower id (one block-wide count per expert); its list index is the
+  // count of active experts with a lower id.
+  if (a.tile_order) {
+    if (ACE_PLAN_LPT && !__syncthreads_or(tid < N && tcnt[tid] > 1)) {
+      for (int e = g; e < N; e += G) {
+        const int ce = cnt[e];
+        const int pos = __syncthreads_count(tid < N && (cnt[tid] > ce || (cnt[tid] == ce && tid < e)));
+        const int idx = __syncthreads_count(tid < e && cnt[tid] > 0);
+        if (tid == 0 && ce > 0) a.tile_order[pos] = idx;
+      }
+    } else if (g == 0) {
+      for (int i = tid; i < toff[N]; i += 256) a.tile_order[i] = i;
+    }
+  }
   // this chunk's kept slots: row = offsets[e] + chunk base of e + rank in the chunk
   if (kept) {
     const int row = off[e_slot] + base[e_slot] + rank;
@@ -248,12 +273,19 @@ __global__ __launch_bounds__(256) void plan_kernel(PlanArgs a) {
 
 }  // namespace
 
-hipError_t launch_plan(const PlanArgs &a, hipStream_t stream) {
-  // one-kernel plan: small matrix, rows of whole words, 16-bit lane sums that cannot overflow
+// one-kernel plan: small matrix, rows of whole words, 16-bit lane sums that cannot overflow
+static bool plan_one_kernel(const PlanArgs &a) {
   const long long bytes = static_cast<long long>(a.G) * a.N;
   const int V = a.N % 16 == 0 ? 4 : 1;
   const int R = a.N % 4 == 0 ? 256 / (a.N / 4 / V) : 0;
-  if (bytes <= kPlanMaxBytes && R > 0 && 16LL * ((a.G + R - 1) / R) <= 0xffff) {
+  return bytes <= kPlanMaxBytes && R > 0 && 16LL * ((a.G + R - 1) / R) <= 0xffff;
+}
+
+bool plan_writes_order(const PlanArgs &a) { return plan_one_kernel(a); }
+
+hipError_t launch_plan(const PlanArgs &a, hipStream_t stream) {
+  const int V = a.N % 16 == 0 ? 4 : 1;
+  if (plan_one_kernel(a)) {
     if (V == 4)
       plan_kernel<4><<<dim3(a.G), 256, 0, stream>>>(a);
     else

@@ -71,6 +71,7 @@ __device__ __forceinline__ TileInfo tile_info(const GemmArgs &a, int grp) {
     ti.once = a.dense_rows <= kTileM;
   } else {
     const int nr = a.n_tiles[0];
+    if (a.tile_order && grp < nr) grp = a.tile_order[grp];
     ti.valid = grp < nr;
     ti.e = ti.valid ? a.tile_expert[grp] : 0;
     ti.row0 = ti.valid ? a.tile_row0[grp] : 0;
