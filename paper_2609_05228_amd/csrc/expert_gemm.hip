@@ -30,7 +30,8 @@
 //    as 4 x 2: a wave owns a quarter of the row blocks (interleaved, so short
 //    tiles stay balanced) and two column groups (gate/up: gate and up blocks of
 //    the same 16 features, so SwiGLU happens in registers; down: 32 columns).
-// fp32 path: plain tiled FMA (small parity workloads).
+// fp32 path: fp32 MFMA (v_mfma_f32_16x16x4f32) on LDS-staged operands (small
+// parity workloads).
 //
 // Launch order is XCD-aware: workgroups are dealt to the 8 XCDs round-robin, so
 // block b runs on XCD b % 8; the N tiles of one M tile are mapped to one XCD so
@@ -312,10 +313,15 @@ __global__ __launch_bounds__(W * 64) void grouped_gemm_bf16_kernel(GemmArgs a) {
     gemm_tile<GATEUP, 16, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
 }
 
-// ------------------------------------------------------------------ fp32 (tiled FMA)
+// ------------------------------------------------------------------ fp32 (MFMA)
+// fp32 layers (the small parity workloads): v_mfma_f32_16x16x4f32 on fp32
+// operands staged in LDS 16 k at a time.  A workgroup (4 waves) takes one M tile
+// (up to 256 rows) and one N tile of 16 features (gate/up: a gate block and an
+// up block) or 16 output columns (down); wave w multiplies row blocks w, w+4,
+// w+8, w+12.  Operand lanes: A row l%16 / B column l%16, k = l/16 of the
+// instruction's 4.
 constexpr int F_BN = 16;
 constexpr int F_BK = 16;
-constexpr int F_RPT = kTileM / 16;  // rows per thread
 
 __global__ __launch_bounds__(256) void gateup_f32_kernel(GemmArgs a) {
   const int nN = a.m / F_BN;
@@ -326,14 +332,15 @@ __global__ __launch_bounds__(256) void gateup_f32_kernel(GemmArgs a) {
   __shared__ float As[kTileM][F_BK + 1];
   __shared__ float Bg[F_BN][F_BK + 1];
   __shared__ float Bu[F_BN][F_BK + 1];
-  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int d = a.d, m = a.m, f0 = nt * F_BN;
+  const int nrb = (ti.rows + 15) >> 4;
   const float *xn = static_cast<const float *>(a.act);
   const float *wg = static_cast<const float *>(a.w0);
   const float *wu = static_cast<const float *>(a.w1);
-  float ag[F_RPT], au[F_RPT];
+  f32x4_t accg[4], accu[4];
 #pragma unroll
-  for (int i = 0; i < F_RPT; ++i) ag[i] = au[i] = 0.f;
+  for (int i = 0; i < 4; ++i) accg[i] = accu[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int k0 = 0; k0 < d; k0 += F_BK) {
     for (int c = tid; c < kTileM * F_BK; c += 256) {
       const int r = c >> 4, kk = c & 15;
@@ -352,22 +359,28 @@ __global__ __launch_bounds__(256) void gateup_f32_kernel(GemmArgs a) {
     }
     __syncthreads();
 #pragma unroll
-    for (int kk = 0; kk < F_BK; ++kk) {
-      const float bgv = Bg[tx][kk], buv = Bu[tx][kk];
+    for (int j = 0; j < F_BK / 4; ++j) {
+      const float bgv = Bg[r16][4 * j + g], buv = Bu[r16][4 * j + g];
 #pragma unroll
-      for (int i = 0; i < F_RPT; ++i) {
-        ag[i] = fmaf(As[ty + 16 * i][kk], bgv, ag[i]);
-        au[i] = fmaf(As[ty + 16 * i][kk], buv, au[i]);
+      for (int i = 0; i < 4; ++i) {
+        const int rb = wave + 4 * i;
+        if (rb >= nrb) break;  // wave-uniform
+        const float av = As[rb * 16 + r16][4 * j + g];
+        accg[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bgv, accg[i], 0, 0, 0);
+        accu[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, buv, accu[i], 0, 0, 0);
       }
     }
     __syncthreads();
   }
+  // lane holds feature f0 + r16 of rows 16 rb + 4 g + q
   float *H = static_cast<float *>(a.out);
 #pragma unroll
-  for (int i = 0; i < F_RPT; ++i) {
-    const int r = ty + 16 * i;
-    if (r < ti.rows) H[static_cast<size_t>(ti.row0 + r) * m + f0 + tx] = silu(ag[i]) * au[i];
-  }
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = (wave + 4 * i) * 16 + 4 * g + q;
+      if (r < ti.rows) H[static_cast<size_t>(ti.row0 + r) * m + f0 + r16] = silu(accg[i][q]) * accu[i][q];
+    }
 }
 
 __global__ __launch_bounds__(256) void down_f32_kernel(GemmArgs a) {
@@ -378,13 +391,14 @@ __global__ __launch_bounds__(256) void down_f32_kernel(GemmArgs a) {
   if (!ti.valid) return;
   __shared__ float As[kTileM][F_BK + 1];
   __shared__ float Bs[F_BN][F_BK + 1];
-  const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, r16 = lane & 15, g = lane >> 4;
   const int d = a.d, m = a.m, n0 = nt * F_BN;
+  const int nrb = (ti.rows + 15) >> 4;
   const float *H = static_cast<const float *>(a.act);
   const float *wd = static_cast<const float *>(a.w0);
-  float acc[F_RPT];
+  f32x4_t acc[4];
 #pragma unroll
-  for (int i = 0; i < F_RPT; ++i) acc[i] = 0.f;
+  for (int i = 0; i < 4; ++i) acc[i] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   for (int k0 = 0; k0 < m; k0 += F_BK) {
     for (int c = tid; c < kTileM * F_BK; c += 256) {
       const int r = c >> 4, kk = c & 15;
@@ -396,19 +410,25 @@ __global__ __launch_bounds__(256) void down_f32_kernel(GemmArgs a) {
     }
     __syncthreads();
 #pragma unroll
-    for (int kk = 0; kk < F_BK; ++kk) {
-      const float bv = Bs[tx][kk];
+    for (int j = 0; j < F_BK / 4; ++j) {
+      const float bv = Bs[r16][4 * j + g];
 #pragma unroll
-      for (int i = 0; i < F_RPT; ++i) acc[i] = fmaf(As[ty + 16 * i][kk], bv, acc[i]);
+      for (int i = 0; i < 4; ++i) {
+        const int rb = wave + 4 * i;
+        if (rb >= nrb) break;  // wave-uniform
+        acc[i] = __builtin_amdgcn_mfma_f32_16x16x4f32(As[rb * 16 + r16][4 * j + g], bv, acc[i], 0, 0, 0);
+      }
     }
     __syncthreads();
   }
   float *Y = static_cast<float *>(a.out);
 #pragma unroll
-  for (int i = 0; i < F_RPT; ++i) {
-    const int r = ty + 16 * i;
-    if (r < ti.rows) Y[static_cast<size_t>(ti.row0 + r) * d + n0 + tx] = acc[i];
-  }
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = (wave + 4 * i) * 16 + 4 * g + q;
+      if (r < ti.rows) Y[static_cast<size_t>(ti.row0 + r) * d + n0 + r16] = acc[i][q];
+    }
 }
 
 unsigned grid_for(int max_groups, int nN) {

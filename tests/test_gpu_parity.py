@@ -94,6 +94,23 @@ def test_small_f32_ragged():
     _report("small f32 ragged", r)
 
 
+@pytest.mark.parametrize("T,N,k,q,m_shared", [(600, 4, 2, 0.5, 0), (1200, 2, 1, 0.0, 0), (600, 6, 2, 0.3, 128)],
+                         ids=["150_rows", "three_tiles", "shared_dense"])
+def test_f32_tall_tiles(T, N, k, q, m_shared):
+    """fp32 layers whose experts hold 150 to 1200 rows (every row block of a 256-row
+    M tile and experts over several tiles), and a dense shared expert over 600 tokens
+    (three M tiles): every output row against the oracle."""
+    name = "zipf_256" if m_shared else "tiny_f32"
+    L = synth.make_layer(synth.config(name, T=T, d=128, N=N, k=k, m=64, m_shared=m_shared, dtype="f32",
+                                      seed=90 + T + N))
+    tb = oracle.tables.build_tables(L)
+    tau = _taus(L, tb["a_gsp"], tb["a_rcr"], [q])[q] if q > 0 else 0.0
+    r = full_check(L, device_layer(L), tb["a_gsp"], tb["a_rcr"], tau)
+    rows = np.bincount(r["gpu"]["topk_idx"][r["gpu"]["keep"].astype(bool)], minlength=N)
+    _report(f"f32 tall tiles T={T} N={N} k={k} q={q} ms={m_shared} rows/expert={rows.tolist()}", r)
+    assert rows.max() > 128
+
+
 # ------------------------------------------------------------------ fusion and single-view variants
 @pytest.mark.parametrize("fusion", ["min", "mean", "gsp", "rcr", "score"])
 def test_fusion_variants_bf16(fusion):
