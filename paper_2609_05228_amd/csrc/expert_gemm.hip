@@ -143,14 +143,18 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   const int na = fav > wave ? (fav - wave + W - 1) / W : 0;
   const int ur = lane >> 3;  // DMA lane -> row in its unit
 
-  // A units this wave stages: u = wave + W j -> row block u / 2, row half u % 2 (= wave % 2)
-  const bf16_t *asrc[NAM];
+  // A units this wave stages: u = wave + W j -> row block u / 2, row half u % 2 (=
+  // wave % 2).  Their token rows come through perm (routed tiles).  The perm loads
+  // are issued from inline assembly ahead of the weight prologue and waited for
+  // explicitly after it: a compiler-placed wait for them would be a vmcnt(0),
+  // which also waits for the weight DMAs issued in between and so holds the
+  // activation prologue back by a whole memory round trip.
+  int srow[NAM];
 #pragma unroll
   for (int j = 0; j < NAM; ++j) {
     const int u = min(wave + W * j, P::FA - 1);
     const int row = min((u >> 1) * 16 + (u & 1) * 8 + ur, ti.rows - 1);  // rows past the tile repeat its last row
-    const int src_row = perm ? perm[ti.row0 + row] : ti.row0 + row;
-    asrc[j] = act + static_cast<size_t>(src_row) * K + 8 * unit_chunk(lane, u & 1);
+    srow[j] = perm ? gload_i32(perm + ti.row0 + row) : ti.row0 + row;
   }
   // B units this wave stages: b = wave * NB + t -> block b / 2, row half t % 2
   const bf16_t *bsrc[NB];
@@ -208,6 +212,17 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   for (int s = 0; s < SB - 1 && s < nk; ++s) {
     const uint32_t st = ldsB + s * P::BSZ;
     issue_b(st, s);
+  }
+  if (perm) {
+    wait_vmcnt(min(SB - 1, nk) * NB);  // the perm loads, issued before these weight DMAs
+#pragma unroll
+    for (int j = 0; j < NAM; ++j) reg_ready(srow[j]);
+  }
+  const bf16_t *asrc[NAM];
+#pragma unroll
+  for (int j = 0; j < NAM; ++j) {
+    const int u = min(wave + W * j, P::FA - 1);
+    asrc[j] = act + static_cast<size_t>(srow[j]) * K + 8 * unit_chunk(lane, u & 1);
   }
   for (int s = 0; s < SA - 1 && s < nk; ++s) {
     const uint32_t st = ldsA + s * P::ASZ;

@@ -64,6 +64,16 @@ __device__ __forceinline__ void dma16_stream(const void *src, uint32_t lds_base)
 
 __device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
 
+// A 32-bit load the compiler does not track: it places no wait for it.  The
+// caller waits with wait_vmcnt (counting this load in its issue order) and then
+// passes the value through reg_ready before reading it.
+__device__ __forceinline__ int gload_i32(const int32_t *p) {
+  int v;
+  asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+__device__ __forceinline__ void reg_ready(int &v) { asm volatile("" : "+v"(v)::"memory"); }
+
 // wait until at most n (0..63) of this wave's vector memory operations are outstanding
 __device__ __forceinline__ void wait_vmcnt(int n) {
 #define ACE_VMCNT_CASE(c) \
