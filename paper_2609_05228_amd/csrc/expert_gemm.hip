@@ -112,8 +112,8 @@ template <int CG> constexpr int stage_halves() { return 2; }
 // b = 2 (2 fg + cb) + j (column group fg, block cb (gate/up: 0 gate, 1 up;
 // down: the group's two 16-column halves), row half j), wave w staging
 // b = w*NB .. w*NB+NB-1.  Inside a unit, row r's 16-byte chunk c sits in slot
-// c ^ r ^ j, so the MFMA fragment reads (16 rows, one chunk each) hit distinct
-// banks.  Wave w computes row blocks wr, wr+RW, ... (wr = w/2) against the CG/2
+// c ^ r (both units of a block alike), so the MFMA fragment reads (16 rows, one
+// chunk each) run at the full LDS rate.  Wave w computes row blocks wr, wr+RW, ... (wr = w/2) against the CG/2
 // column groups starting at wc*CG/2 (wc = w%2).
 template <bool GATEUP, int MB, int CG, int KH, int W>
 __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, int erot, uint8_t *smem) {
@@ -124,7 +124,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   constexpr int MW = MB / RW;  // row blocks per wave
   constexpr int CW = CG / 2;   // column groups per wave
   constexpr int BN = GATEUP ? 16 * CG : 32 * CG;  // tile width (features or output columns)
-  static_assert(NB % 2 == 0 && W % 2 == 0, "a wave's units must keep one row half");
+  static_assert(W % 2 == 0, "waves form an RW x 2 grid");
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g = lane >> 4;
@@ -163,7 +163,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     const int b = wave * NB + t;
     const int blk = b >> 1, j = b & 1;
     const int fg = blk >> 1, cb = blk & 1;
-    const int c = 8 * unit_chunk(lane, j);
+    const int c = 8 * unit_chunk(lane);
     if (GATEUP) {
       const size_t f = static_cast<size_t>(ti.e) * a.m + nt * BN + fg * 16 + 8 * j + ur;
       bsrc[t] = static_cast<const bf16_t *>(cb ? w1 : w0) + f * a.d + c;
@@ -222,7 +222,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
 #pragma unroll
   for (int j = 0; j < NAM; ++j) {
     const int u = min(wave + W * j, P::FA - 1);
-    asrc[j] = act + static_cast<size_t>(srow[j]) * K + 8 * unit_chunk(lane, u & 1);
+    asrc[j] = act + static_cast<size_t>(srow[j]) * K + 8 * unit_chunk(lane);
   }
   for (int s = 0; s < SA - 1 && s < nk; ++s) {
     const uint32_t st = ldsA + s * P::ASZ;

@@ -3,12 +3,16 @@
 //
 // An "8-row unit" is what one DMA instruction moves: 8 rows x 128 bytes (a
 // 64-wide bf16 K stage of 8 rows, whole cache lines).  DMA lane i lands at
-// byte 16*i, i.e. row i/8, slot i%8; the lane fetches chunk (i%8) ^ (i/8) ^ j
-// of its row, j being the unit's half (0 or 1) of a 16-row MFMA block, so
-// chunk c of row r sits in slot c ^ r ^ j.  A 16-row block is two consecutive
-// units; lane l's operand of v_mfma_f32_16x16x32_bf16 (row l%16, 8 k values
-// 32h + 8(l/16) .. +7 of k half h) is then read from unit_read_offset(l, h),
-// and the 16 lanes of a read phase hit distinct banks.
+// byte 16*i, i.e. row i/8, slot i%8; the lane fetches chunk (i%8) ^ (i/8) of
+// its row, so chunk c of row r sits in slot c ^ r.  A 16-row block is two
+// consecutive units with the same permutation; lane l's operand of
+// v_mfma_f32_16x16x32_bf16 (row l%16, 8 k values 32h + 8(l/16) .. +7 of k half
+// h) is read from unit_read_offset(l, h).  Measured on gfx950 (ds_read_b128,
+// 8 waves per CU): this read pattern runs at the full LDS rate (~236 bytes per
+// clock per CU, as for 16 lanes reading one contiguous 256-byte block) at any
+// 1 KB-aligned block base; giving the second unit another permutation (slot c ^
+// r ^ 1, which is bank-distinct under a plain address-modulo bank map) halves
+// it, so the bank map evidently folds in address bits above the 256-byte row.
 #pragma once
 
 #include "ace_internal.h"
@@ -21,13 +25,14 @@ __device__ __forceinline__ uint32_t lds_addr(const void *p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void *)p));
 }
 
-// chunk (16 bytes, 8 bf16) of its row that DMA lane `lane` fetches in a unit of half j
-__device__ __forceinline__ int unit_chunk(int lane, int j) { return (lane & 7) ^ (lane >> 3) ^ j; }
+// chunk (16 bytes, 8 bf16) of its row that DMA lane `lane` fetches (either unit
+// of a 16-row block)
+__host__ __device__ inline int unit_chunk(int lane) { return (lane & 7) ^ (lane >> 3); }
 
 // byte offset, from a 16-row block's first unit, of lane's MFMA operand for k half h
-__device__ __forceinline__ int unit_read_offset(int lane, int h) {
+__host__ __device__ inline int unit_read_offset(int lane, int h) {
   const int r16 = lane & 15, g = lane >> 4, rlo = r16 & 7, uh = r16 >> 3;
-  return uh * kUnitBytes + rlo * 128 + (((4 * h + g) ^ rlo ^ uh) << 4);
+  return uh * kUnitBytes + rlo * 128 + (((4 * h + g) ^ rlo) << 4);
 }
 
 // 16 bytes per lane from global `src` into LDS at lds_base + 16 * lane.  M0 is

@@ -207,7 +207,7 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
 #pragma unroll
   for (int t = 0; t < 4; ++t) {
     const int cb = t >> 1, j = t & 1;
-    const int c = kbase + 8 * unit_chunk(lane, j);
+    const int c = kbase + 8 * unit_chunk(lane);
     if (GATEUP) {
       const size_t f = static_cast<size_t>(ti.e) * a.m + nb * 16 + 8 * j + ur;
       src[t] = static_cast<const bf16_t *>(cb ? a.w1 : a.w0) + f * a.d + c;
@@ -225,7 +225,7 @@ __device__ __forceinline__ void skinny_item(const SkinnyArgs &sa, const TileInfo
     // self_plan: the token of tile row r sits in lane r of tok (tile rows <= 64;
     // this item covers tile rows rbase ..)
     const int src_row = sa.self_plan ? __shfl(tok, rbase + row) : a.perm ? a.perm[ti.row0 + row] : ti.row0 + row;
-    src[t] = act + static_cast<size_t>(src_row) * K + kbase + 8 * unit_chunk(lane, j);
+    src[t] = act + static_cast<size_t>(src_row) * K + kbase + 8 * unit_chunk(lane);
   }
   const uint32_t ring_lds = lds_addr(ring);
   // Stage st covers the 64-wide K block (st + k0) % nk of this split: waves start
