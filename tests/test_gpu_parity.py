@@ -86,6 +86,22 @@ def test_small_bf16_zipf_shared():
     _report("small zipf + shared", r)
 
 
+@pytest.mark.parametrize("T,q", [(1300, 0.5), (1100, 0.0)], ids=["T1300_q0.5", "T1100_q0"])
+def test_bf16_shared_in_routed_tall(T, q):
+    """bf16 wider-pool layer whose shared expert has the routed experts' size, so its
+    M tiles join the routed grouped-GEMM launches; the Zipf router gives the hottest
+    experts several 256-row tiles plus a partial one and the shared expert T % 256
+    rows in its last tile: every tile of the launch order (full tiles by list order,
+    then partial tiles by rows) is exercised, and y is checked on every token."""
+    L = synth.make_layer(synth.config("zipf_256", T=T, d=256, N=16, k=4, m=128, m_shared=128, seed=5))
+    tb = oracle.tables.build_tables(L)
+    tau = _taus(L, tb["a_gsp"], tb["a_rcr"], [q])[q]
+    r = full_check(L, device_layer(L), tb["a_gsp"], tb["a_rcr"], tau)
+    counts = np.bincount(r["gpu"]["topk_idx"][r["gpu"]["keep"].astype(bool)], minlength=16)
+    _report(f"bf16 shared-in-routed T={T} q={q} rows/expert={counts.tolist()}", r)
+    assert counts.max() > 2 * 256 and counts.max() % 256 != 0 and T % 256 != 0
+
+
 def test_small_f32_ragged():
     L = synth.make_layer(synth.config("tiny_f32", T=77, d=128, N=12, k=3, m=64, seed=3))
     tb = oracle.tables.build_tables(L)
