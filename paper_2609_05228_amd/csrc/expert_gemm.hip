@@ -29,7 +29,9 @@
 //  * 8 waves (two per SIMD, so one wave's LDS reads overlap the other's MFMAs)
 //    as 4 x 2: a wave owns a quarter of the row blocks (interleaved, so short
 //    tiles stay balanced) and two column groups (gate/up: gate and up blocks of
-//    the same 16 features, so SwiGLU happens in registers; down: 32 columns).
+//    the same 16 features, so SwiGLU happens in registers; down: 32 columns);
+//  * the down launch gives each workgroup two N tiles of one M tile, run as one
+//    pipeline (the second tile's first stages load under the first's last steps).
 // fp32 path: fp32 MFMA (v_mfma_f32_16x16x4f32) on LDS-staged operands (small
 // parity workloads).
 //
@@ -103,6 +105,43 @@ template <int CG> constexpr int stage_halves() { return 2; }
 // Pipe, cum_ops and pending_ok (gemm_pipe.h): ring depths per tile shape and
 // the exact wait counts of a wave's DMA issue sequence.
 
+// Output stores of gemm_tile: lane holds column r16 of each block, rows 4*g + q.
+template <bool GATEUP, int MW, int CW, int RW, int BN>
+__device__ __forceinline__ void store_tile_impl(const GemmArgs &a, const TileInfo &ti, void *outp,
+                                                f32x4_t (&acc)[MW][2 * CW], int nt, int wr, int wc, int r16, int g) {
+#pragma unroll
+  for (int fl = 0; fl < CW; ++fl) {
+    const int grp = wc * CW + fl;
+    if (GATEUP) {
+      bf16_t *H = static_cast<bf16_t *>(outp);
+      const int f = nt * BN + grp * 16 + r16;
+#pragma unroll
+      for (int i = 0; i < MW; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = (wr + RW * i) * 16 + 4 * g + q;
+          if (row < ti.rows)
+            H[static_cast<size_t>(ti.row0 + row) * a.m + f] =
+                f32_to_bf16(silu_for_bf16(acc[i][fl * 2][q]) * acc[i][fl * 2 + 1][q]);
+        }
+    } else {
+      bf16_t *Y = static_cast<bf16_t *>(outp);
+      const int n = nt * BN + grp * 32 + r16;
+#pragma unroll
+      for (int i = 0; i < MW; ++i)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = (wr + RW * i) * 16 + 4 * g + q;
+          if (row < ti.rows) {
+            bf16_t *yr = Y + static_cast<size_t>(ti.row0 + row) * a.d + n;
+            yr[0] = f32_to_bf16(acc[i][fl * 2][q]);
+            yr[16] = f32_to_bf16(acc[i][fl * 2 + 1][q]);
+          }
+        }
+    }
+  }
+}
+
 // One M tile x one N tile with MB 16-row blocks, CG column groups and KH = 2
 // k halves per stage (64-wide stages: 128 bytes of every row).  One DMA
 // instruction moves an 8-row unit: 8 rows x 128 bytes, each row a whole cache
@@ -116,7 +155,8 @@ template <int CG> constexpr int stage_halves() { return 2; }
 // chunk each) run at the full LDS rate.  Wave w computes row blocks wr, wr+RW, ... (wr = w/2) against the CG/2
 // column groups starting at wc*CG/2 (wc = w%2).
 template <bool GATEUP, int MB, int CG, int KH, int W>
-__device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt, int erot, uint8_t *smem) {
+__device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt0, int ntiles, int erot,
+                                          uint8_t *smem) {
   static_assert(KH == 2, "8-row DMA units span a 64-wide K stage");
   using P = Pipe<MB, CG, KH, W>;
   constexpr int RW = W / 2;    // waves along the rows
@@ -165,10 +205,10 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     const int fg = blk >> 1, cb = blk & 1;
     const int c = 8 * unit_chunk(lane);
     if (GATEUP) {
-      const size_t f = static_cast<size_t>(ti.e) * a.m + nt * BN + fg * 16 + 8 * j + ur;
+      const size_t f = static_cast<size_t>(ti.e) * a.m + nt0 * BN + fg * 16 + 8 * j + ur;
       bsrc[t] = static_cast<const bf16_t *>(cb ? w1 : w0) + f * a.d + c;
     } else {
-      const size_t n = static_cast<size_t>(ti.e) * a.d + nt * BN + fg * 32 + cb * 16 + 8 * j + ur;
+      const size_t n = static_cast<size_t>(ti.e) * a.d + nt0 * BN + fg * 32 + cb * 16 + 8 * j + ur;
       bsrc[t] = static_cast<const bf16_t *>(w0) + n * a.m + c;
     }
   }
@@ -184,8 +224,17 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   for (int i = 0; i < MW; ++i)
 #pragma unroll
     for (int c = 0; c < 2 * CW; ++c) acc[i][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  auto store_tile = [&](f32x4_t (&ac)[MW][2 * CW], int nt) {
+    store_tile_impl<GATEUP, MW, CW, RW, BN>(a, ti, outp, ac, nt, wr, wc, r16, g);
+  };
 
   const int nk = K / BK;
+  // ntiles (1 or 2) N tiles of the M tile, nt0 and nt0 + 1, run as one pipeline
+  // of NK = ntiles * nk stages: stage s is K block s % nk of tile s / nk, so the
+  // second tile's first stages are in flight while the first tile's last steps
+  // and its output stores run (no second prologue ramp)
+  const int NK = ntiles * nk;
+  const size_t tile_step = static_cast<size_t>(BN) * K;  // weight elements from one N tile to the next
   // Pipeline stage s covers K block (s + k0) % nk, k0 set by the tile's expert.
   // Experts start at different K blocks: rows 4 KB apart (d = 2048 bf16) read at
   // one K offset by every workgroup at once concentrate on a few HBM channels and
@@ -195,26 +244,30 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   // (starting each M tile at its own block left them out of step, and the
   // wider-pool gate/up fetched three times its weight bytes from beyond L2).
   const int k0 = erot % nk;
-  auto kofs = [&](int s) { return (s + k0 < nk ? s + k0 : s + k0 - nk) * BK; };
+  auto kofs = [&](int s) {
+    s = s < nk ? s : s - nk;
+    return (s + k0 < nk ? s + k0 : s + k0 - nk) * BK;
+  };
   // weight units of stage s into LDS stage base st: weights that no other M tile
   // reads stream with the non-temporal hint; weights shared by several M tiles
   // (large experts, the dense expert's tiles) stay cacheable for the other tiles
   auto issue_b = [&](uint32_t st, int s) {
+    const size_t o = (s < nk ? 0 : tile_step) + kofs(s);
     if (ti.once) {
 #pragma unroll
-      for (int t = 0; t < NB; ++t) dma16_stream(bsrc[t] + kofs(s), st + (wave * NB + t) * kFragBytes);
+      for (int t = 0; t < NB; ++t) dma16_stream(bsrc[t] + o, st + (wave * NB + t) * kFragBytes);
     } else {
 #pragma unroll
-      for (int t = 0; t < NB; ++t) dma16(bsrc[t] + kofs(s), st + (wave * NB + t) * kFragBytes);
+      for (int t = 0; t < NB; ++t) dma16(bsrc[t] + o, st + (wave * NB + t) * kFragBytes);
     }
   };
   // prologue: B stages 0..SB-2, then A stages 0..SA-2
-  for (int s = 0; s < SB - 1 && s < nk; ++s) {
+  for (int s = 0; s < SB - 1 && s < NK; ++s) {
     const uint32_t st = ldsB + s * P::BSZ;
     issue_b(st, s);
   }
   if (perm) {
-    wait_vmcnt(min(SB - 1, nk) * NB);  // the perm loads, issued before these weight DMAs
+    wait_vmcnt(min(SB - 1, NK) * NB);  // the perm loads, issued before these weight DMAs
 #pragma unroll
     for (int j = 0; j < NAM; ++j) reg_ready(srow[j]);
   }
@@ -224,17 +277,17 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     const int u = min(wave + W * j, P::FA - 1);
     asrc[j] = act + static_cast<size_t>(srow[j]) * K + 8 * unit_chunk(lane);
   }
-  for (int s = 0; s < SA - 1 && s < nk; ++s) {
+  for (int s = 0; s < SA - 1 && s < NK; ++s) {
     const uint32_t st = ldsA + s * P::ASZ;
 #pragma unroll
     for (int j = 0; j < NAM; ++j)
       if (j < na) dma16(asrc[j] + kofs(s), st + (wave + W * j) * kFragBytes);
   }
 
-  for (int kt = 0; kt < nk; ++kt) {
-    wait_vmcnt(pending_ok<P>(kt, nk, na));
+  for (int kt = 0; kt < NK; ++kt) {
+    wait_vmcnt(pending_ok<P>(kt, NK, na));
     barrier();  // stage kt landed for every wave; every wave is done with stage kt-1
-    if (kt + SA - 1 < nk) {
+    if (kt + SA - 1 < NK) {
       const int s = kt + SA - 1;
       const uint32_t st = ldsA + (s % SA) * P::ASZ;
 #pragma unroll
@@ -263,55 +316,35 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       // MFMAs, so their issue (the memory pipeline's back-pressure) overlaps the
       // matrix cores instead of delaying them; the issue order, and so every
       // vmcnt count, is unchanged (A of a step, then its B)
-      if (h == 0 && kt + SB - 1 < nk) {
+      if (h == 0 && kt + SB - 1 < NK) {
         const int s = kt + SB - 1;
         issue_b(ldsB + (s % SB) * P::BSZ, s);
       }
     }
-  }
-
-  // epilogue: lane holds column r16 of each block, rows 4*g + q
-#pragma unroll
-  for (int fl = 0; fl < CW; ++fl) {
-    const int grp = wc * CW + fl;
-    if (GATEUP) {
-      bf16_t *H = static_cast<bf16_t *>(outp);
-      const int f = nt * BN + grp * 16 + r16;
+    if (kt == nk - 1 && ntiles > 1) {
+      store_tile(acc, nt0);
 #pragma unroll
       for (int i = 0; i < MW; ++i)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = (wr + RW * i) * 16 + 4 * g + q;
-          if (row < ti.rows)
-            H[static_cast<size_t>(ti.row0 + row) * a.m + f] =
-                f32_to_bf16(silu_for_bf16(acc[i][fl * 2][q]) * acc[i][fl * 2 + 1][q]);
-        }
-    } else {
-      bf16_t *Y = static_cast<bf16_t *>(outp);
-      const int n = nt * BN + grp * 32 + r16;
-#pragma unroll
-      for (int i = 0; i < MW; ++i)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int row = (wr + RW * i) * 16 + 4 * g + q;
-          if (row < ti.rows) {
-            bf16_t *yr = Y + static_cast<size_t>(ti.row0 + row) * a.d + n;
-            yr[0] = f32_to_bf16(acc[i][fl * 2][q]);
-            yr[16] = f32_to_bf16(acc[i][fl * 2 + 1][q]);
-          }
-        }
+        for (int c = 0; c < 2 * CW; ++c) acc[i][c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     }
   }
+  store_tile(acc, nt0 + ntiles - 1);
 }
 
 // tile width in features (gate/up) or output columns (down) for CG column groups
 template <bool GATEUP> constexpr int tile_width(int cg) { return GATEUP ? 16 * cg : 32 * cg; }
 
-template <bool GATEUP, int CG, int W>
+// TPW (1 or 2): N tiles per workgroup, consecutive tiles of one M tile in one
+// pipeline (gemm_tile).
+template <bool GATEUP, int CG, int W, int TPW>
 __global__ __launch_bounds__(W * 64) void grouped_gemm_bf16_kernel(GemmArgs a) {
+  static_assert(TPW == 1 || TPW == 2, "one or two N tiles per workgroup");
   const int nN = (GATEUP ? a.m : a.d) / tile_width<GATEUP>(CG);
-  int grp, nt;
-  map_block(blockIdx.x, nN, &grp, &nt);
+  const int nP = (nN + TPW - 1) / TPW;
+  int grp, np;
+  map_block(blockIdx.x, nP, &grp, &np);
+  const int nt0 = np * TPW, ntiles = min(TPW, nN - nt0);
   const TileInfo ti = tile_info(a, grp);
   if (!ti.valid) return;
   __shared__ __align__(16) uint8_t smem[kLdsBytes];
@@ -319,13 +352,13 @@ __global__ __launch_bounds__(W * 64) void grouped_gemm_bf16_kernel(GemmArgs a) {
   // K rotation key: the expert (the appended dense expert gets its own)
   const int erot = ti.sh ? 0x155 : ti.e;
   if (blocks <= 4)
-    gemm_tile<GATEUP, 4, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
+    gemm_tile<GATEUP, 4, CG, stage_halves<CG>(), W>(a, ti, nt0, ntiles, erot, smem);
   else if (blocks <= 8)
-    gemm_tile<GATEUP, 8, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
+    gemm_tile<GATEUP, 8, CG, stage_halves<CG>(), W>(a, ti, nt0, ntiles, erot, smem);
   else if (blocks <= 12)
-    gemm_tile<GATEUP, 12, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
+    gemm_tile<GATEUP, 12, CG, stage_halves<CG>(), W>(a, ti, nt0, ntiles, erot, smem);
   else
-    gemm_tile<GATEUP, 16, CG, stage_halves<CG>(), W>(a, ti, nt, erot, smem);
+    gemm_tile<GATEUP, 16, CG, stage_halves<CG>(), W>(a, ti, nt0, ntiles, erot, smem);
 }
 
 // ------------------------------------------------------------------ fp32 (MFMA)
@@ -446,6 +479,15 @@ __global__ __launch_bounds__(256) void down_f32_kernel(GemmArgs a) {
     }
 }
 
+// N tiles per workgroup.  Down: two (K is only m deep, so a tile is a short
+// pipeline; the pair runs as one and the grid is one round of workgroups fewer:
+// wider-pool down 153.9 -> 149.3 us, the 4096-token layer's unchanged).  Gate/up:
+// one (two made it 8-12% slower: 768 tiles as 384 workgroups leave half of the
+// CUs idle in the second round).
+constexpr int kTpwGateUp = 1;
+constexpr int kTpwDown = 2;
+int pairs(int nN, int tpw) { return (nN + tpw - 1) / tpw; }
+
 unsigned grid_for(int max_groups, int nN) {
   const int g8 = (max_groups + 7) / 8;
   return static_cast<unsigned>(8 * nN * g8);
@@ -459,11 +501,13 @@ hipError_t launch_gateup(const GemmArgs &a, bool bf16, hipStream_t stream) {
   {
     // 128 features per tile when they divide m, else 64
     if (a.m % tile_width<true>(8) == 0)
-      grouped_gemm_bf16_kernel<true, 8, kGemmWaves>
-          <<<dim3(grid_for(a.max_groups, a.m / tile_width<true>(8))), kGemmWaves * 64, 0, stream>>>(a);
+      grouped_gemm_bf16_kernel<true, 8, kGemmWaves, kTpwGateUp>
+          <<<dim3(grid_for(a.max_groups, pairs(a.m / tile_width<true>(8), kTpwGateUp))), kGemmWaves * 64, 0,
+             stream>>>(a);
     else
-      grouped_gemm_bf16_kernel<true, 4, kGemmWaves>
-          <<<dim3(grid_for(a.max_groups, a.m / tile_width<true>(4))), kGemmWaves * 64, 0, stream>>>(a);
+      grouped_gemm_bf16_kernel<true, 4, kGemmWaves, kTpwGateUp>
+          <<<dim3(grid_for(a.max_groups, pairs(a.m / tile_width<true>(4), kTpwGateUp))), kGemmWaves * 64, 0,
+             stream>>>(a);
   }
   else
     gateup_f32_kernel<<<dim3(grid_for(a.max_groups, a.m / F_BN)), 256, 0, stream>>>(a);
@@ -476,11 +520,13 @@ hipError_t launch_down(const GemmArgs &a, bool bf16, hipStream_t stream) {
   {
     // 256 output columns per tile when they divide d, else 128
     if (a.d % tile_width<false>(8) == 0)
-      grouped_gemm_bf16_kernel<false, 8, kGemmWaves>
-          <<<dim3(grid_for(a.max_groups, a.d / tile_width<false>(8))), kGemmWaves * 64, 0, stream>>>(a);
+      grouped_gemm_bf16_kernel<false, 8, kGemmWaves, kTpwDown>
+          <<<dim3(grid_for(a.max_groups, pairs(a.d / tile_width<false>(8), kTpwDown))), kGemmWaves * 64, 0,
+             stream>>>(a);
     else
-      grouped_gemm_bf16_kernel<false, 4, kGemmWaves>
-          <<<dim3(grid_for(a.max_groups, a.d / tile_width<false>(4))), kGemmWaves * 64, 0, stream>>>(a);
+      grouped_gemm_bf16_kernel<false, 4, kGemmWaves, kTpwDown>
+          <<<dim3(grid_for(a.max_groups, pairs(a.d / tile_width<false>(4), kTpwDown))), kGemmWaves * 64, 0,
+             stream>>>(a);
   }
   else
     down_f32_kernel<<<dim3(grid_for(a.max_groups, a.d / F_BN)), 256, 0, stream>>>(a);
