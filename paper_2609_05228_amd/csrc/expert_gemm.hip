@@ -273,10 +273,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
   }
   const bf16_t *asrc[NAM];
 #pragma unroll
-  for (int j = 0; j < NAM; ++j) {
-    const int u = min(wave + W * j, P::FA - 1);
-    asrc[j] = act + static_cast<size_t>(srow[j]) * K + 8 * unit_chunk(lane);
-  }
+  for (int j = 0; j < NAM; ++j) asrc[j] = act + static_cast<size_t>(srow[j]) * K + 8 * unit_chunk(lane);
   for (int s = 0; s < SA - 1 && s < NK; ++s) {
     const uint32_t st = ldsA + s * P::ASZ;
 #pragma unroll
