@@ -65,6 +65,11 @@ SMALL = [
     (130, 384, 64, 8, 128, 1, 0.5),
     (257, 256, 256, 8, 64, 2, 0.25),
     (515, 128, 40, 6, 320, 1, 0.6),
+    # 17-256 router chunks with 113-256 experts: the router's LDS-staged logits
+    # (expert rows past N and token rows past T repeat the last; d * 2 bytes of
+    # gamma not a whole number of 1 KB units)
+    (1000, 384, 120, 8, 128, 1, 0.5),
+    (600, 256, 200, 6, 64, 2, 0.4),
 ]
 
 
