@@ -50,8 +50,8 @@ ZIPF_TABLES = os.path.join(ROOT, "tests", "golden", "tables_zipf_256_seed0.json"
 STACK_TABLES = os.path.join(ROOT, "tests", "golden", "tables_stack_48_seed0.json")
 TRAFFIC = os.path.join(ROOT, "profiles", "prefill_4096_traffic.json")
 # stage -> (kernel name in the rocprofv3 traffic record, source file)
-STAGE_KERNEL = {"gateup": ("grouped_gemm_bf16_kernel<true, 8, 8>", "expert_gemm.hip"),
-                "down": ("grouped_gemm_bf16_kernel<false, 8, 8>", "expert_gemm.hip"),
+STAGE_KERNEL = {"gateup": ("grouped_gemm_bf16_kernel<true, 8, 8, 1>", "expert_gemm.hip"),
+                "down": ("grouped_gemm_bf16_kernel<false, 8, 8, 2>", "expert_gemm.hip"),
                 "route": ("route_kernel<unsigned short, 8, false>", "route.hip"),
                 "combine": ("combine_kernel<unsigned short>", "combine.hip")}
 
