@@ -142,8 +142,9 @@ __device__ __forceinline__ void store_tile_impl(const GemmArgs &a, const TileInf
   }
 }
 
-// One M tile x one N tile with MB 16-row blocks, CG column groups and KH = 2
-// k halves per stage (64-wide stages: 128 bytes of every row).  One DMA
+// One M tile x ntiles (1 or 2) consecutive N tiles from nt0, with MB 16-row
+// blocks, CG column groups and KH = 2 k halves per stage (64-wide stages: 128
+// bytes of every row).  One DMA
 // instruction moves an 8-row unit: 8 rows x 128 bytes, each row a whole cache
 // line (16-row x 64-byte fragments touch twice as many lines per instruction and
 // stream measurably slower).  A stage of A holds units u = 2 rb + j (row block
@@ -152,8 +153,8 @@ __device__ __forceinline__ void store_tile_impl(const GemmArgs &a, const TileInf
 // down: the group's two 16-column halves), row half j), wave w staging
 // b = w*NB .. w*NB+NB-1.  Inside a unit, row r's 16-byte chunk c sits in slot
 // c ^ r (both units of a block alike), so the MFMA fragment reads (16 rows, one
-// chunk each) run at the full LDS rate.  Wave w computes row blocks wr, wr+RW, ... (wr = w/2) against the CG/2
-// column groups starting at wc*CG/2 (wc = w%2).
+// chunk each) run at the full LDS rate.  Wave w computes row blocks wr, wr+RW,
+// ... (wr = w/2) against the CG/2 column groups starting at wc*CG/2 (wc = w%2).
 template <bool GATEUP, int MB, int CG, int KH, int W>
 __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti, int nt0, int ntiles, int erot,
                                           uint8_t *smem) {
