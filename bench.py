@@ -58,13 +58,19 @@ STAGE_KERNEL = {"gateup": ("grouped_gemm_bf16_kernel<true, 8, 8, 1>", "expert_ge
 
 def source_digest(src: str) -> str:
     """First 16 hex digits of sha256 over a kernel's source file and every shared
-    header of the sources: the key that ties a traffic record to the code."""
+    header of the sources, comments and blank space removed (a comment edit leaves
+    the code, and so the record, valid): the key that ties a traffic record to
+    the code."""
     import hashlib
+    import re
 
     csrc = os.path.join(ROOT, "paper_2609_05228_amd", "csrc")
     h = hashlib.sha256()
     for f in [src] + sorted(n for n in os.listdir(csrc) if n.endswith(".h")):
-        h.update(open(os.path.join(csrc, f), "rb").read())
+        text = open(os.path.join(csrc, f), encoding="utf-8").read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)  # block comments
+        text = re.sub(r"//[^\n]*", " ", text)                # line comments
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
