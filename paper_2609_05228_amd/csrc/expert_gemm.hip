@@ -301,14 +301,24 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       for (int c = 0; c < 2 * CW; ++c)
         bf[c] = *reinterpret_cast<const bf16x8_t *>(sb + (2 * (wc * CW + (c >> 1)) + (c & 1)) * 2 * kFragBytes +
                                                     (h ? rd_off1 : rd_off0));
+      // every row block's fragment is read up front, with the weight fragments
+      // (blocks past the tile read stale LDS and are not multiplied): a read
+      // placed after the branch below made each row block's MFMAs wait a full
+      // LDS round trip
+      bf16x8_t av[MW];
+#pragma unroll
+      for (int i = 0; i < MW; ++i)
+        av[i] = *reinterpret_cast<const bf16x8_t *>(sa + (wr + RW * i) * 2 * kFragBytes + (h ? rd_off1 : rd_off0));
+      // an empty use here keeps the compiler from sinking each read into the
+      // branch that multiplies it
+#pragma unroll
+      for (int i = 0; i < MW; ++i) asm volatile("" ::"v"(av[i]));
 #pragma unroll
       for (int i = 0; i < MW; ++i) {
         if ((wr + RW * i) * 16 >= ti.rows) break;  // wave-uniform: row blocks past the tile
-        const bf16x8_t av =
-            *reinterpret_cast<const bf16x8_t *>(sa + (wr + RW * i) * 2 * kFragBytes + (h ? rd_off1 : rd_off0));
 #pragma unroll
         for (int c = 0; c < 2 * CW; ++c)
-          acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bf[c], acc[i][c], 0, 0, 0);
+          acc[i][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[i], bf[c], acc[i][c], 0, 0, 0);
       }
       // the weight DMAs of stage kt + SB - 1 go out behind the first k half's
       // MFMAs, so their issue (the memory pipeline's back-pressure) overlaps the
