@@ -449,11 +449,18 @@ __device__ __forceinline__ void plan_one_chunk(const RouteArgs &a, const uint32_
 // group, lane `sub` holding slot `sub` (sub < k); zrow = the token's N logits
 // in LDS.  Writes the token's routing outputs; returns the expert and keep
 // decision of this lane's slot through my_e / my_kept.
+// top (or nullptr): the token's k keys in selection order, already chosen.
 template <int NT>
 __device__ __forceinline__ void select_token(const RouteArgs &a, const float *zrow, int t, bool tvalid, int sub,
-                                             const float *a_gsp_s, const float *a_rcr_s, int &my_e, bool &my_kept) {
+                                             const float *a_gsp_s, const float *a_rcr_s, int &my_e, bool &my_kept,
+                                             const uint64_t *top = nullptr) {
   const int N = a.N;
   const int k = a.k;
+  uint64_t mykey = 0, topkey = 0;
+  if (top) {
+    topkey = top[0];
+    if (sub < k) mykey = top[sub];
+  } else {
   // this lane's candidates, experts sub + 16 q, sorted; it can lose at most k <= 8 of them
   uint64_t cand[NT];
 #pragma unroll
@@ -468,7 +475,6 @@ __device__ __forceinline__ void select_token(const RouteArgs &a, const float *zr
   for (int q = 0; q < L; ++q) head[q] = cand[q];
   // k rounds: the row maximum of the lanes' heads is the next slot; the lane
   // that held it pops its head
-  uint64_t mykey = 0, topkey = 0;
 #pragma unroll
   for (int i = 0; i < kMaxK; ++i) {
     if (i >= k) break;
@@ -479,6 +485,7 @@ __device__ __forceinline__ void select_token(const RouteArgs &a, const float *zr
 #pragma unroll
     for (int q = 0; q + 1 < L; ++q) head[q] = win ? head[q + 1] : head[q];
     head[L - 1] = win ? 0ull : head[L - 1];
+  }
   }
   const bool slot = sub < k;
   const int se = slot ? key_expert(mykey) : 0;  // this lane's slot: expert and logit
@@ -532,7 +539,16 @@ __device__ __forceinline__ void select_token(const RouteArgs &a, const float *zr
   }
 }
 
-template <typename T, int NT, bool SPLIT>
+// One-token top-k by rank (route_kernel): NC slices of JL experts each, NC * NP
+// <= 512 threads, one (expert, slice) pair per thread.
+template <int NP> struct RankSlices {
+  static constexpr int JL = NP * NP / 512 > 1 ? NP * NP / 512 : 1;
+  static constexpr int NC = NP / JL;
+  static_assert(NC * JL == NP && NC * NP <= 512, "slices cover the experts");
+};
+
+// ONE (with SPLIT): a batch of one token, its top-k by rank.
+template <typename T, int NT, bool SPLIT, bool ONE = false>
 __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   constexpr int NP = NT * 16;
   const T *__restrict__ x = static_cast<const T *>(a.x);
@@ -544,6 +560,8 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   __shared__ float rstd_s[kTok];
   __shared__ uint32_t emask[NP];
   __shared__ float a_gsp_s[NP], a_rcr_s[NP];
+  __shared__ uint64_t key_s[ONE ? NP : 1], top_s[ONE ? kMaxK : 1];  // one-token top-k by rank
+  __shared__ uint16_t rank_s[ONE ? RankSlices<NP>::NC : 1][ONE ? NP : 1];
   static_assert(512 % NP == 0, "a thread meets one expert column in the logits reduction");
 
   const int tid = threadIdx.x;
@@ -612,6 +630,32 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
       zred[0][tl][e] = zred[0][tl][e] * rstd_s[tl] + bias;
     }
     __syncthreads();
+    if constexpr (ONE) {
+      // one token (batch 1): its top-k by rank.  Expert i's rank is the number of
+      // keys above its key (keys are distinct, so the ranks are a permutation and
+      // ranks 0..k-1 are the top-k in selection order); the 512 threads each
+      // count over a slice of the experts, a few dozen independent comparisons
+      // instead of the 16-lane sort and arg-max rounds' dependent chain
+      constexpr int JL = RankSlices<NP>::JL, NC = RankSlices<NP>::NC;  // experts per slice, slices
+      if (tid < NP) key_s[tid] = tid < N ? topk_key(zred[0][0][tid], tid) : 0ull;
+      __syncthreads();
+      const int i = tid % NP, c = tid / NP;
+      const uint64_t ki = key_s[i];
+      if (c < NC) {
+        int r = 0;
+#pragma unroll 8
+        for (int jj = 0; jj < JL; ++jj) r += key_s[c * JL + jj] > ki ? 1 : 0;
+        rank_s[c][i] = static_cast<uint16_t>(r);
+      }
+      __syncthreads();
+      if (tid < N) {
+        int rr = 0;
+#pragma unroll
+        for (int q = 0; q < NC; ++q) rr += rank_s[q][tid];
+        if (rr < a.k) top_s[rr] = ki;
+      }
+      __syncthreads();
+    }
   } else {
     // ---- 1. logits over all K: wave w takes blocks w, w + 8, ...
     // workgroups are dealt to the 8 XCDs round-robin: rotate by the index on the XCD
@@ -664,7 +708,8 @@ __global__ __launch_bounds__(512) void route_kernel(RouteArgs a) {
   } else {
     // ---- 2. top-k, gates and Alg. 4 (waves 0-3): one token per 16-lane
     // group, lane `sub` holds slot `sub` (sub < k)
-    select_token<NT>(a, zred[0][tl], t, t < nt, sub, a_gsp_s, a_rcr_s, my_e, my_kept);
+    select_token<NT>(a, zred[0][tl], t, t < nt, sub, a_gsp_s, a_rcr_s, my_e, my_kept,
+                     ONE ? top_s : nullptr);
   }
   // ---- per-expert token masks of this chunk -> local ranks and counts
   if (my_kept) atomicOr(&emask[my_e], 1u << tl);
@@ -903,7 +948,10 @@ void launch_route_nt(const RouteArgs &a, hipStream_t stream) {
   }
   if (a.ksplit > 0) {
     route_partial_kernel<T, NT><<<dim3(chunks, a.ksplit), 256, 0, stream>>>(a);
-    route_kernel<T, NT, true><<<dim3(chunks), 512, 0, stream>>>(a);
+    if (a.T == 1)
+      route_kernel<T, NT, true, true><<<dim3(chunks), 512, 0, stream>>>(a);
+    else
+      route_kernel<T, NT, true><<<dim3(chunks), 512, 0, stream>>>(a);
   } else {
     route_kernel<T, NT, false><<<dim3(chunks), 512, 0, stream>>>(a);
   }
