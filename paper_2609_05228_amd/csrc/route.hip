@@ -25,7 +25,8 @@
 //     partial logits, and the per-chunk kernel adds the slices.
 //  2. Selection (waves 0-3, one token per 16-lane group, lane i holds slot i):
 //     top-k by k rounds of a 16-lane arg-max on DPP row rotations (ties go to
-//     the lower expert id), gates g = exp(z_i - z_1) / sum_j exp(z_j - z_1)
+//     the lower expert id; a batch of one token instead ranks every expert's
+//     key against the others with all 512 threads), gates g = exp(z_i - z_1) / sum_j exp(z_j - z_1)
 //     over the k selected logits (the softmax over all N experts cancels in
 //     the renormalised gate), then Alg. 4 with 16-lane sums.  For the dispatch
 //     plan each kept slot gets its rank among this chunk's kept slots of the
