@@ -14,6 +14,10 @@ from . import _lib
 
 _DT = {torch.bfloat16: _lib.ACE_BF16, torch.float32: _lib.ACE_F32}
 _WS_CACHE: dict = {}
+# superseded cached workspaces stay allocated: a HIP graph captured with one of them
+# keeps its device address, so freeing it when a larger layer call grows the cache
+# would let a replay of that graph write into memory the allocator has handed out again
+_WS_RETIRED: list = []
 
 
 def _ptr(t):
@@ -45,11 +49,15 @@ def make_desc(T, d, N, k, m, dtype, tau, m_min=1, eps=1e-6, rms_eps=1e-6, n_shar
 
 
 def workspace(desc: _lib.Desc, device) -> torch.Tensor:
-    """A cached uint8 device buffer of ace_moe_workspace_size(desc) bytes."""
+    """A cached uint8 device buffer of at least ace_moe_workspace_size(desc) bytes, one
+    per (device, stream); calls on one stream share it in stream order.  When a call
+    needs more, a larger buffer replaces it and the old one is kept, never freed."""
     n = _lib.workspace_size(desc)
     key = (str(device), torch.cuda.current_stream(device).cuda_stream)
     buf = _WS_CACHE.get(key)
     if buf is None or buf.numel() < n:
+        if buf is not None:
+            _WS_RETIRED.append(buf)
         buf = torch.empty(max(n, 256), dtype=torch.uint8, device=device)
         _WS_CACHE[key] = buf
     return buf
