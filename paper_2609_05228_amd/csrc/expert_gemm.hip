@@ -490,8 +490,11 @@ __global__ __launch_bounds__(256) void down_f32_kernel(GemmArgs a) {
 // N tiles per workgroup.  Down: two (K is only m deep, so a tile is a short
 // pipeline; the pair runs as one and the grid is one round of workgroups fewer:
 // wider-pool down 153.9 -> 149.3 us, the 4096-token layer's unchanged).  Gate/up:
-// one (two made it 8-12% slower: 768 tiles as 384 workgroups leave half of the
-// CUs idle in the second round).
+// one.  Two, three or four made it 9-50% slower, three even where its grid is
+// exactly one round on the 256 CUs: with one tile per workgroup the N tiles of an
+// M tile run at once on one XCD and share the gathered activation rows in its L2,
+// while a workgroup walking its tiles one after the other gathers them again for
+// each tile.
 constexpr int kTpwGateUp = 1;
 constexpr int kTpwDown = 2;
 int pairs(int nN, int tpw) { return (nN + tpw - 1) / tpw; }
