@@ -108,27 +108,46 @@ def log(msg: str) -> None:
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def event_times(fns, steps: int, warmup: int, torch, ace):
-    """Per-step ms of `steps` layer calls after `warmup` untimed ones, and the average
-    ms per stage.  fns is one callable or a list cycled through (one per seeded input).
-    The library records HIP events on the layer's stream before its first stage and
-    after each stage of every timed call (timing-only events, created without a
-    system-scope fence, so they do not flush the caches between stages); a step's time
-    is the span from its first to its last event, i.e. the layer from RMSNorm to the
-    combine, and the stage times come from the same timed calls."""
+def event_times(fns, steps: int, warmup: int, torch, ace, stages: bool = True, settle_ms: float = 200.0):
+    """Per-step ms of `steps` layer calls after untimed ones (calls for about settle_ms,
+    so that the clocks settle after the host-side work that preceded the leg, then
+    `warmup` calls), and the average ms per stage (None with stages=False).  fns is
+    one callable or a list cycled through (one per seeded input).  The library records timing-only HIP events
+    (created without a system-scope fence, so they do not flush the caches) on the
+    layer's stream.  Two timed passes of `steps` calls: in the first each call records
+    only an event before RMSNorm and one after the combine, and a step's time is that
+    span (the layer with no intermediate records, each of which costs the stream about
+    a microsecond); in the second each call also records an event after every stage,
+    which gives the stage times (their sum exceeds the span by those records)."""
     fns = fns if isinstance(fns, (list, tuple)) else [fns]
+    t0 = time.perf_counter()
+    i = 0
+    while (time.perf_counter() - t0) * 1e3 < settle_ms:
+        fns[i % len(fns)]()
+        i += 1
+        if i % 10 == 0:
+            torch.cuda.synchronize()
     for i in range(warmup):
         fns[i % len(fns)]()
     torch.cuda.synchronize()
-    ace.profile_begin(steps)
-    try:
-        for i in range(steps):
-            fns[i % len(fns)]()
-    finally:
-        tot, n, calls = ace.profile_end(steps)
-    torch.cuda.synchronize()
-    assert n == steps, (n, steps)
-    return [sum(c.values()) for c in calls], {k: v / max(n, 1) for k, v in tot.items()}
+
+    def timed(span):
+        ace.profile_begin(steps, span=span)
+        try:
+            for i in range(steps):
+                fns[i % len(fns)]()
+        finally:
+            tot, n, calls = ace.profile_end(steps)
+        torch.cuda.synchronize()
+        assert n == steps, (n, steps)
+        return tot, calls
+
+    _, calls = timed(True)
+    ms = [sum(c.values()) for c in calls]
+    if not stages:
+        return ms, None
+    tot, _ = timed(False)
+    return ms, {k: v / steps for k, v in tot.items()}
 
 
 def summary(ms_list) -> dict:
@@ -330,9 +349,10 @@ def main():
     tabs = (torch.tensor(gold["a_gsp"], dtype=torch.float32, device=dev),
             torch.tensor(gold["a_rcr"], dtype=torch.float32, device=dev))
 
-    def prefill_leg(tau_, skip_disable=False, steps=None, warmup=None, stages=True):
+    def prefill_leg(tau_, skip_disable=False, steps=None, warmup=None, stages=True, settle_ms=200.0):
         fn, o, _ = make_step(D["x"], D, tabs, k, tau_, skip_disable)
-        ms_list, st = event_times(fn, steps or args.steps, args.warmup if warmup is None else warmup, torch, ace)
+        ms_list, st = event_times(fn, steps or args.steps, args.warmup if warmup is None else warmup, torch, ace,
+                                  stages=stages, settle_ms=settle_ms)
         s = summary(ms_list)
         keep = o["keep"].cpu().numpy()
         counts = o["counts"].cpu().numpy()
@@ -361,7 +381,7 @@ def main():
                 f, o, ws = make_step(xs[s], D, tabs, k, tau, ws=ws)
                 fa.append(f)
                 outs.append(o)
-            eager_a, _ = event_times(fa, S, min(args.warmup, S), torch, ace)
+            eager_a, _ = event_times(fa, S, min(args.warmup, S), torch, ace, stages=False)
             ms_a = graph_steps(fa, 20)
             kb = np.stack([o["keep"].cpu().numpy() for o in outs])
             ib = np.stack([o["topk_idx"].cpu().numpy() for o in outs])
@@ -388,7 +408,7 @@ def main():
                     f, o, ws = make_step(xs[s], D, tabs, k, tau, skip_disable=True, ws=ws)
                     ft.append(f)
                     outs_t.append(o)
-                eager_t, _ = event_times(ft, S, min(args.warmup, S), torch, ace)
+                eager_t, _ = event_times(ft, S, min(args.warmup, S), torch, ace, stages=False)
                 st_, set_ = summary(graph_steps(ft, 20)), summary(eager_t)
                 ea_t = np.array([int((o["counts"].cpu().numpy() > 0).sum()) for o in outs_t])
                 r.update({"topk_ms_per_step": round(st_["median"], 5),
@@ -420,7 +440,8 @@ def main():
         s_top, o_top, _ = make_step(ZW["x"], ZW, zt, zcfg.k, ztau, skip_disable=True, ws=ws)
         ms_a, st = event_times(s_ace, args.steps, args.warmup, torch, ace)
         # --ace-only (profiler runs): the plain layer once, untimed, for its expert count only
-        ms_t = [float("nan")] if args.ace_only else event_times(s_top, args.steps, args.warmup, torch, ace)[0]
+        ms_t = ([float("nan")] if args.ace_only
+                else event_times(s_top, args.steps, args.warmup, torch, ace, stages=False)[0])
         if args.ace_only:
             s_top()
         sa, stt = summary(ms_a), summary(ms_t)
@@ -517,12 +538,13 @@ def main():
 
         def timed_passes(chain, inputs):
             """Each pass over the chain (one per input) with the library's timing events
-            on every layer call: MoE ms of a pass = the sum of its layer calls' spans;
-            the whole pass (copy-in, layers, residual adds) is bracketed by two events."""
+            on every layer call (only before its first and after its last stage): MoE ms
+            of a pass = the sum of its layer calls' spans; the whole pass (copy-in,
+            layers, residual adds) is bracketed by two events."""
             run_chain(chain, inputs[0])  # warm-up
             torch.cuda.synchronize()
             ends = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in inputs]
-            ace.profile_begin(n_layers * len(inputs))
+            ace.profile_begin(n_layers * len(inputs), span=True)
             try:
                 for (a, b), xi in zip(ends, inputs):
                     a.record()
@@ -680,7 +702,7 @@ def main():
     del pw_fn
     log(f"prewarm: {n_pw} untimed layer calls in {(time.perf_counter() - t0) * 1e3:.0f} ms")
     log(f"timing prefill: {args.warmup} warmup + {args.steps} steps")
-    head, ace_out, stages = prefill_leg(tau)
+    head, ace_out, stages = prefill_leg(tau, settle_ms=0.0)
     ms = head["ms_per_step"]
     n_kept, e_act = head["kept_slots"], head["experts_active"]
     log(f"prefill {ms:.4f} ms/step (median), skip {head['realised_skip']}, E_act {e_act}, stages {stages}")
@@ -708,8 +730,10 @@ def main():
                    "T": T, "d": d, "N": N, "k": k, "m": m, "skip_target": float(args.q), "tau": tau,
                    "realised_skip": head["realised_skip"], "experts_active": e_act, "kept_slots": n_kept},
         "timing": {"method": "per step, the span of the library's timing-only HIP events (no system fence) "
-                             "on the layer's stream from before RMSNorm to after the combine; "
-                             "ms_per_step = median over the timed steps",
+                             "on the layer's stream from before RMSNorm to after the combine, with no event "
+                             "between the stages; ms_per_step = median over the timed steps. The stage times "
+                             "come from a second pass of as many steps with an event after every stage "
+                             "(stage_sum_ms: their sum, which includes those records)",
                    "mean_ms": head["mean_ms"], "min_ms": head["min_ms"], "max_ms": head["max_ms"],
                    "stage_sum_ms": head["stage_sum_ms"], "step_ms": head.pop("step_ms")},
         "stages_ms": head["stages_ms"],

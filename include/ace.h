@@ -32,7 +32,7 @@
 extern "C" {
 #endif
 
-#define ACE_ABI_VERSION 4
+#define ACE_ABI_VERSION 5
 
 typedef enum {
   ACE_OK = 0,
@@ -189,9 +189,14 @@ ace_status ace_moe_forward_noalloc(const ace_moe_desc *desc, const void *x, cons
  * without a system-scope fence (timing only), so recording them does not flush
  * the caches between stages.  Only one profile may be open per process; begin
  * while open -> ACE_ERR_INVALID_ARG.
+ * ace_profile_begin_span(max_calls) opens the same profile, but each call records
+ * only its first and its last event: a call's time is the span of the whole layer
+ * without the intermediate records (each one costs the stream about a
+ * microsecond), and ace_profile_end reports all of it as the last stage's.
  */
 #define ACE_PROFILE_STAGES 6
 ace_status ace_profile_begin(int max_calls);
+ace_status ace_profile_begin_span(int max_calls);
 ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls, double *call_stage_ms, int max_calls);
 
 /*

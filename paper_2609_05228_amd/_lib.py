@@ -81,6 +81,8 @@ def lib() -> ctypes.CDLL:
         L.ace_abi_version.restype = ctypes.c_int
         L.ace_profile_begin.argtypes = [ctypes.c_int]
         L.ace_profile_begin.restype = ctypes.c_int
+        L.ace_profile_begin_span.argtypes = [ctypes.c_int]
+        L.ace_profile_begin_span.restype = ctypes.c_int
         L.ace_profile_end.argtypes = [ctypes.POINTER(ctypes.c_double), ctypes.c_int,
                                       ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_double),
                                       ctypes.c_int]
@@ -113,8 +115,11 @@ def abi_version() -> int:
 PROFILE_STAGES = ("route", "plan", "gateup", "down", "shared", "combine")
 
 
-def profile_begin(max_calls: int) -> None:
-    st = int(lib().ace_profile_begin(int(max_calls)))
+def profile_begin(max_calls: int, span: bool = False) -> None:
+    """Open a stage-timing profile of the next max_calls layer calls; span=True records
+    only each call's first and last event (its whole time, reported as the last stage)."""
+    fn = lib().ace_profile_begin_span if span else lib().ace_profile_begin
+    st = int(fn(int(max_calls)))
     if st != ACE_OK:
         raise AceError(st, status_string(st))
 

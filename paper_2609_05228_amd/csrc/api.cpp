@@ -151,6 +151,7 @@ ace_status validate(const ace_moe_desc *d, const void *x, const ace_moe_weights 
 struct Profile {
   std::mutex mu;
   bool on = false;
+  bool span = false;  // record only the first and the last event of each call
   int cap = 0;
   int used = 0;
   std::vector<hipEvent_t> ev;  // cap x (stages + 1)
@@ -163,19 +164,20 @@ constexpr int kStages = ACE_PROFILE_STAGES;
 struct ProfSlot {
   hipEvent_t *ev = nullptr;
   uint8_t *rec = nullptr;
+  bool span = false;
 };
 ProfSlot profile_slot() {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (!g_prof.on || g_prof.used >= g_prof.cap) return {};
   const size_t o = static_cast<size_t>(g_prof.used++) * (kStages + 1);
   std::fill(g_prof.rec.begin() + o, g_prof.rec.begin() + o + kStages + 1, uint8_t{0});
-  return {&g_prof.ev[o], &g_prof.rec[o]};
+  return {&g_prof.ev[o], &g_prof.rec[o], g_prof.span};
 }
 
 // event i after stage i-1; `launched` = false for a stage that enqueued nothing, whose
 // time then counts as zero (each record costs the stream a few microseconds)
 void mark(const ProfSlot &slot, int i, hipStream_t s, bool launched = true) {
-  if (slot.ev && (launched || i == 0 || i == kStages)) {
+  if (slot.ev && ((launched && !slot.span) || i == 0 || i == kStages)) {
     (void)hipEventRecord(slot.ev[i], s);
     slot.rec[i] = 1;
   }
@@ -215,15 +217,7 @@ hipError_t scratch_on_current_device(void **out) {
   return hipSuccess;
 }
 
-ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
-                        const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
-                        void *stream_ptr);
-
-}  // namespace
-
-extern "C" {
-
-ace_status ace_profile_begin(int max_calls) {
+ace_status profile_open(int max_calls, bool span) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
   if (g_prof.on || max_calls <= 0 || max_calls > 100000) return ACE_ERR_INVALID_ARG;
   g_prof.ev.assign(static_cast<size_t>(max_calls) * (kStages + 1), nullptr);
@@ -240,9 +234,22 @@ ace_status ace_profile_begin(int max_calls) {
   g_prof.rec.assign(g_prof.ev.size(), uint8_t{0});
   g_prof.cap = max_calls;
   g_prof.used = 0;
+  g_prof.span = span;
   g_prof.on = true;
   return ACE_OK;
 }
+
+ace_status forward_impl(const ace_moe_desc *desc, const void *x, const ace_moe_weights *w,
+                        const ace_moe_outputs *out, void *workspace, size_t workspace_bytes,
+                        void *stream_ptr);
+
+}  // namespace
+
+extern "C" {
+
+ace_status ace_profile_begin(int max_calls) { return profile_open(max_calls, false); }
+
+ace_status ace_profile_begin_span(int max_calls) { return profile_open(max_calls, true); }
 
 ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls, double *call_stage_ms, int max_calls) {
   std::lock_guard<std::mutex> lk(g_prof.mu);
@@ -279,6 +286,7 @@ ace_status ace_profile_end(double *stage_ms, int n_stages, int *n_calls, double 
   g_prof.ev.clear();
   g_prof.rec.clear();
   g_prof.on = false;
+  g_prof.span = false;
   g_prof.cap = g_prof.used = 0;
   return st;
 }
