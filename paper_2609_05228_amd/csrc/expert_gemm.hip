@@ -282,8 +282,13 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       if (j < na) dma16(asrc[j] + kofs(s), st + (wave + W * j) * kFragBytes);
   }
 
+  using SS = Steady<P>;
+  const int ss_hi = SS::hi(NK);
   for (int kt = 0; kt < NK; ++kt) {
-    wait_vmcnt(pending_ok<P>(kt, NK, na));
+    if (SS::on && na > 0 && kt >= SS::lo && kt < ss_hi)
+      wait_vmcnt(SS::pending);
+    else
+      wait_vmcnt(pending_ok<P>(kt, NK, na));
     barrier();  // stage kt landed for every wave; every wave is done with stage kt-1
     if (kt + SA - 1 < NK) {
       const int s = kt + SA - 1;

@@ -2,7 +2,8 @@
 // shape the kernels instantiate, every K length up to 128 stages and every per-wave
 // activation DMA count, replay the wave's DMA issue sequence one instruction at a
 // time and compare pending_ok with the count of DMAs issued after the later of
-// A(kt) and B(kt) at the wait before stage kt (vmcnt completes in issue order).
+// A(kt) and B(kt) at the wait before stage kt (vmcnt completes in issue order),
+// and the steady-state constant (Steady) with it wherever the kernels use it.
 // Also checks that both stages were issued before their wait, that the count fits
 // the 0..63 wait table, and that a refilled ring slot held the stage consumed in
 // the previous iteration.  Prints "ok" and exits 0, else the first mismatch.
@@ -33,6 +34,12 @@ static bool check() {
         if (got != want || got < 0 || got > 63) {
           std::printf("MB=%d CG=%d KH=%d nk=%d na=%d kt=%d: pending_ok %d, replay %d\n", MB, CG, KH, nk, na, kt, got,
                       want);
+          return false;
+        }
+        using SS = ace::Steady<P>;
+        if (SS::on && na > 0 && kt >= SS::lo && kt < SS::hi(nk) && want != SS::pending) {
+          std::printf("MB=%d CG=%d KH=%d nk=%d na=%d kt=%d: steady-state count %d, replay %d\n", MB, CG, KH, nk, na,
+                      kt, SS::pending, want);
           return false;
         }
         // slots refilled in this iteration held stage kt - 1 (consumed before the barrier)
