@@ -21,8 +21,9 @@
 //    through two LDS rings in 160 KB: activations (L2-resident) 2-4 K stages deep,
 //    expert weights (from HBM; with the non-temporal hint when no other M tile
 //    reads them) 3-8 stages deep; each wave waits only for the
-//    stage it computes next (vmcnt counted exactly from the issue schedule), then
-//    one barrier per K step;
+//    stage it computes next (vmcnt counted exactly from the issue schedule; a
+//    constant in the steady state, since a run-time count becomes a branch tree
+//    that costs matrix-bound tiles several percent), then one barrier per K step;
 //  * one DMA instruction moves 8 rows x 128 bytes (whole cache lines) and lane i
 //    lands at byte 16*i; the chunk a lane fetches is XOR-swizzled by its row so
 //    the MFMA fragment reads (16 rows x 16 bytes) are bank-conflict free;
