@@ -482,8 +482,8 @@ def check_plan():
 
 
 # --------------------------------------------------------------------------- tie accounting
-# Hand-built tokens for each decision margin the parity tests excuse (the benchmark spec: ties
-# within 1e-6 are counted): the top-k boundary and the in-top-k slot order (Sec. 3.1,
+# Hand-built tokens for each decision margin the parity tests excuse (decisions within
+# 1e-6 of a margin count as ties): the top-k boundary and the in-top-k slot order (Sec. 3.1,
 # ties to the lower id), the strict c < tau test of a non-top-1 slot (Alg. 4, top-1
 # kept) and, with m_min > 1, the restore order by descending c (Alg. 4).  Logits and
 # contributions are written out here with plain numpy, not taken from the oracle.
