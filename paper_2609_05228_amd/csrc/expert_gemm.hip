@@ -21,9 +21,10 @@
 //    through two LDS rings in 160 KB: activations (L2-resident) 2-4 K stages deep,
 //    expert weights (from HBM; with the non-temporal hint when no other M tile
 //    reads them) 3-8 stages deep; each wave waits only for the
-//    stage it computes next (vmcnt counted exactly from the issue schedule; a
-//    constant in the steady state, since a run-time count becomes a branch tree
-//    that costs matrix-bound tiles several percent), then one barrier per K step;
+//    stage it computes next (vmcnt counted exactly from the issue schedule; with
+//    two activation stages one of two constants, since a run-time count becomes a
+//    branch tree that costs matrix-bound tiles several percent), then one barrier
+//    per K step;
 //  * one DMA instruction moves 8 rows x 128 bytes (whole cache lines) and lane i
 //    lands at byte 16*i; the chunk a lane fetches is XOR-swizzled by its row so
 //    the MFMA fragment reads (16 rows x 16 bytes) are bank-conflict free;
@@ -283,13 +284,16 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
       if (j < na) dma16(asrc[j] + kofs(s), st + (wave + W * j) * kFragBytes);
   }
 
-  using SS = Steady<P>;
-  const int ss_hi = SS::hi(NK);
+  using CF = Closed<P>;
   for (int kt = 0; kt < NK; ++kt) {
-    if (SS::on && na > 0 && kt >= SS::lo && kt < ss_hi)
-      wait_vmcnt(SS::pending);
-    else
+    if (CF::on && na > 0) {
+      if (CF::nb_pending(kt, NK))
+        wait_vmcnt(NB);
+      else
+        wait_vmcnt(0);
+    } else {
       wait_vmcnt(pending_ok<P>(kt, NK, na));
+    }
     barrier();  // stage kt landed for every wave; every wave is done with stage kt-1
     if (kt + SA - 1 < NK) {
       const int s = kt + SA - 1;

@@ -71,16 +71,15 @@ __host__ __device__ inline int pending_ok(int kt, int nk, int na) {
   return cum_ops<P>(kt, nk, na) - pipe_max(end_a, end_b);
 }
 
-// Steady state.  With SA == 2 < SB the later DMA of stage kt is its A DMA, issued in
-// iteration kt - 1 and followed only by that iteration's B DMAs (stage kt + SB - 2),
-// so for every wave that stages A units (na > 0) and every kt in
-// [steady_lo, steady_hi(nk)) the wait count is NB: a constant, which saves the
-// run-time count and its branch tree in most iterations.
-template <class P> struct Steady {
+// Closed form for SA == 2 < SB.  A wave that stages A units (na > 0) issues A(0)
+// last in its prologue and A(kt) as the first DMA of iteration kt - 1, followed in
+// that iteration only by B(kt + SB - 2) when that stage exists; B(kt) always went
+// out earlier.  So the wait before stage kt allows NB DMAs when kt >= 1 and
+// kt + SB - 2 < nk, and none otherwise: two constant waits, which spare the
+// run-time count and its branch tree in every step.
+template <class P> struct Closed {
   static constexpr bool on = P::SA == 2 && P::SB > 2;
-  static constexpr int lo = P::SB - 1;
-  static constexpr int pending = P::NB;
-  __host__ __device__ static int hi(int nk) { return nk - P::SB + 2; }
+  __host__ __device__ static bool nb_pending(int kt, int nk) { return kt >= 1 && kt + P::SB - 2 < nk; }
 };
 
 }  // namespace ace

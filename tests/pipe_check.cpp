@@ -3,7 +3,7 @@
 // activation DMA count, replay the wave's DMA issue sequence one instruction at a
 // time and compare pending_ok with the count of DMAs issued after the later of
 // A(kt) and B(kt) at the wait before stage kt (vmcnt completes in issue order),
-// and the steady-state constant (Steady) with it wherever the kernels use it.
+// and the closed form (Closed) with it wherever the kernels use it.
 // Also checks that both stages were issued before their wait, that the count fits
 // the 0..63 wait table, and that a refilled ring slot held the stage consumed in
 // the previous iteration.  Prints "ok" and exits 0, else the first mismatch.
@@ -36,10 +36,10 @@ static bool check() {
                       want);
           return false;
         }
-        using SS = ace::Steady<P>;
-        if (SS::on && na > 0 && kt >= SS::lo && kt < SS::hi(nk) && want != SS::pending) {
-          std::printf("MB=%d CG=%d KH=%d nk=%d na=%d kt=%d: steady-state count %d, replay %d\n", MB, CG, KH, nk, na,
-                      kt, SS::pending, want);
+        using CF = ace::Closed<P>;
+        if (CF::on && na > 0 && want != (CF::nb_pending(kt, nk) ? P::NB : 0)) {
+          std::printf("MB=%d CG=%d KH=%d nk=%d na=%d kt=%d: closed-form count %d, replay %d\n", MB, CG, KH, nk, na, kt,
+                      CF::nb_pending(kt, nk) ? P::NB : 0, want);
           return false;
         }
         // slots refilled in this iteration held stage kt - 1 (consumed before the barrier)
