@@ -270,7 +270,12 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs &a, const TileInfo &ti,
     issue_b(st, s);
   }
   if (perm) {
-    wait_vmcnt(min(SB - 1, NK) * NB);  // the perm loads, issued before these weight DMAs
+    // the perm loads, issued before these weight DMAs (a constant count unless K is
+    // shorter than the weight prologue)
+    if (NK >= SB - 1)
+      wait_vmcnt((SB - 1) * NB);
+    else
+      wait_vmcnt(NK * NB);
 #pragma unroll
     for (int j = 0; j < NAM; ++j) reg_ready(srow[j]);
   }
