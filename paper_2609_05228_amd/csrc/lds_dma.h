@@ -36,23 +36,21 @@ __host__ __device__ inline int unit_read_offset(int lane, int h) {
 }
 
 // 16 bytes per lane from global `src` into LDS at lds_base + 16 * lane.  M0 is
-// saved and restored around the DMA so the compiler's use of it is unaffected.
+// declared clobbered, so the compiler sets it again wherever it needs it (saving
+// and restoring it around every DMA cost the matrix-bound tiles about 1%).
 // An SALU write of M0 needs one wait state before a global load with the LDS bit
 // reads it (the ISA's table of manually inserted wait states; the compiler's
 // hazard check does not see inside this asm), hence the s_nop.
 // The compiler does not see this LDS write: every consumer waits on vmcnt
 // explicitly (and crosses a barrier when another wave issued the copy).
 __device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
-  uint32_t saved;
   asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
+      "s_mov_b32 m0, %1\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
+      "global_load_lds_dwordx4 %0, off"
+      :
       : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_base))
-      : "memory");
+      : "memory", "m0");
 }
 
 // dma16 with the non-temporal cache hint (nt), for data each launch reads once:
@@ -60,16 +58,13 @@ __device__ __forceinline__ void dma16(const void *src, uint32_t lds_base) {
 // reused data (activation rows, H and Y between kernels, the router rows); the
 // decode GEMMs stream about 10% faster with it.
 __device__ __forceinline__ void dma16_stream(const void *src, uint32_t lds_base) {
-  uint32_t saved;
   asm volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
+      "s_mov_b32 m0, %1\n\t"
       "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off nt\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
+      "global_load_lds_dwordx4 %0, off nt"
+      :
       : "v"(src), "s"(__builtin_amdgcn_readfirstlane(lds_base))
-      : "memory");
+      : "memory", "m0");
 }
 
 __device__ __forceinline__ void barrier() { asm volatile("s_barrier" ::: "memory"); }
